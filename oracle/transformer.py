@@ -1,0 +1,221 @@
+"""The generator p and the reward model s of section 3, in float64.
+
+The paper treats both as black boxes: p is sampled auto-regressively
+(eq. auto-regressive), s maps prompt and response to a real number (section 3,
+"Inference-time Alignment"), evaluated on the concatenation of the prompt and
+a (partial) response (section 4.2, eq. partial-reward-set).  Its models are
+Llama-3-8B and Mistral-7B-shaped decoders (section 5), so both are written
+here as a pre-norm Llama-style decoder:
+
+* h_0 = E[token]
+* per layer: a = RMSNorm(h) * g_attn;  q, k, v = a Wq^T, a Wk^T, a Wv^T;
+  rotate-half RoPE on q and k at the token's absolute position;
+  causal attention with grouped KV heads (query head j reads KV head
+  floor(j * hkv / hq)), scale 1/sqrt(hd);  h += o Wo^T;
+  f = RMSNorm(h) * g_ffn;  h += (silu(f W1^T) * (f W3^T)) W2^T
+* out = RMSNorm(h) * g_final.
+* generator: logits = out W_head^T (untied head);
+  reward model: s = w_head . out[last token] (a scalar head, no bias).
+
+RMSNorm(x) = x / sqrt(mean(x^2) + eps).  RoPE frequency i is
+theta^(-2i/hd); pair (x_i, x_{i+hd/2}) rotates by position * frequency.
+
+Weights come in the packed layout of the C interface: wqkv [nl][(hq+2hkv)hd][d]
+(q rows, then k, then v), wo [nl][d][hq hd], w13 [nl][2][ff][d] (gate, up),
+w2 [nl][d][ff]; bf16 weights as uint16 bit patterns, widened exactly.
+
+The per-candidate decode state keeps a private KV cache for every row,
+prompt included: nothing is shared between candidates here.
+"""
+import numpy as np
+
+
+def widen(a) -> np.ndarray:
+    """Weights as float64 (bf16 bit patterns are widened exactly)."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return a.astype(np.float64)
+
+
+def rmsnorm(x, g, eps):
+    return x / np.sqrt(np.mean(x * x, axis=-1, keepdims=True) + eps) * g
+
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def rope_cos_sin(positions, head_dim, theta):
+    half = head_dim // 2
+    freq = theta ** (-2.0 * np.arange(half, dtype=np.float64) / head_dim)
+    ang = np.asarray(positions, dtype=np.float64)[..., None] * freq
+    return np.cos(ang), np.sin(ang)
+
+
+def rope(x, cos, sin):
+    """Rotate-half RoPE on the last axis; cos/sin broadcast over heads."""
+    half = x.shape[-1] // 2
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+def softmax(x, axis=-1):
+    m = np.max(x, axis=axis, keepdims=True)
+    e = np.exp(x - m)
+    return e / np.sum(e, axis=axis, keepdims=True)
+
+
+def causal_attention(q, k, v, n_kv_heads):
+    """Causal attention of one sequence: q [T][hq][hd], k, v [T][hkv][hd].
+
+    Query head j reads KV head floor(j * hkv / hq); query i sees keys 0..i.
+    """
+    T, hq, hd = q.shape
+    mask = np.triu(np.ones((T, T), dtype=bool), k=1)
+    o = np.empty_like(q)
+    for j in range(hq):
+        kh = (j * n_kv_heads) // hq
+        sc = (q[:, j, :] @ k[:, kh, :].T) / np.sqrt(hd)
+        sc[mask] = -np.inf
+        o[:, j, :] = softmax(sc) @ v[:, kh, :]
+    return o
+
+
+class Transformer:
+    """A decoder given by a shape (see ``synth.ModelShape``) and weights."""
+
+    def __init__(self, shape, weights: dict, reward: bool, cache_f64: bool = None):
+        self.s = shape
+        self.reward = reward
+        self.raw = weights
+        nparams = sum(int(np.prod(np.shape(v))) for v in weights.values())
+        self.cache_f64 = (nparams * 8 < (4 << 30)) if cache_f64 is None else cache_f64
+        self._c = {}
+
+    # -- weight access -------------------------------------------------
+    def w(self, name, layer=None):
+        key = (name, layer)
+        if key in self._c:
+            return self._c[key]
+        a = self.raw[name] if layer is None else self.raw[name][layer]
+        a = widen(a)
+        if self.cache_f64:
+            self._c[key] = a
+        return a
+
+    def _split_qkv(self, qkv):
+        s = self.s
+        nq, nk = s.n_heads * s.head_dim, s.n_kv_heads * s.head_dim
+        q = qkv[..., :nq].reshape(qkv.shape[:-1] + (s.n_heads, s.head_dim))
+        k = qkv[..., nq:nq + nk].reshape(qkv.shape[:-1] + (s.n_kv_heads, s.head_dim))
+        v = qkv[..., nq + nk:].reshape(qkv.shape[:-1] + (s.n_kv_heads, s.head_dim))
+        return q, k, v
+
+    def _ffn(self, h, l):
+        s = self.s
+        f = rmsnorm(h, self.w("ffn_norm", l), s.rms_eps)
+        w13 = self.w("w13", l)
+        gate = f @ w13[0].T
+        up = f @ w13[1].T
+        return (silu(gate) * up) @ self.w("w2", l).T
+
+    def kv_head_of(self, j):
+        return (j * self.s.n_kv_heads) // self.s.n_heads
+
+    # -- full causal forward over one sequence ---------------------------
+    def forward(self, tokens):
+        """Final normalised hidden states [T][d] of one token sequence."""
+        s = self.s
+        tokens = np.asarray(tokens, dtype=np.int64)
+        T = len(tokens)
+        h = self.w("embed")[tokens] if self.cache_f64 else widen(self.raw["embed"][tokens])
+        cos, sin = rope_cos_sin(np.arange(T), s.head_dim, s.rope_theta)
+        cos, sin = cos[:, None, :], sin[:, None, :]
+        for l in range(s.n_layers):
+            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
+            q, k = rope(q, cos, sin), rope(k, cos, sin)
+            o = causal_attention(q, k, v, s.n_kv_heads)
+            h = h + o.reshape(T, -1) @ self.w("wo", l).T
+            h = h + self._ffn(h, l)
+        return rmsnorm(h, self.w("final_norm"), s.rms_eps)
+
+    def logits(self, tokens):
+        """Generator logits [T][V]: row t is the distribution of token t+1."""
+        assert not self.reward
+        return self.forward(tokens) @ self.w("head").T
+
+    def score(self, tokens) -> float:
+        """Reward model s(x, y): scalar head on the last token's state."""
+        assert self.reward
+        out = self.forward(tokens)
+        return float(out[-1] @ self.w("head"))
+
+    # -- batched incremental decoding with private caches ---------------
+    def start(self, prompt, rows: int, capacity: int):
+        """Decode state for ``rows`` candidates that all begin with ``prompt``.
+
+        Every row gets its own copy of the prompt's keys and values (the
+        prompt forward is deterministic, so it is evaluated once and copied).
+        ``capacity`` bounds prompt plus response length.
+        Returns (state, logits of the last prompt position [V]).
+        """
+        s = self.s
+        prompt = np.asarray(prompt, dtype=np.int64)
+        P = len(prompt)
+        h = widen(self.raw["embed"][prompt])
+        cos, sin = rope_cos_sin(np.arange(P), s.head_dim, s.rope_theta)
+        cos, sin = cos[:, None, :], sin[:, None, :]
+        state = {"k": [], "v": [], "pos": P}
+        for l in range(s.n_layers):
+            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
+            q, k = rope(q, cos, sin), rope(k, cos, sin)
+            o = causal_attention(q, k, v, s.n_kv_heads)
+            h = h + o.reshape(P, -1) @ self.w("wo", l).T
+            h = h + self._ffn(h, l)
+            # private per-row caches [rows][kvh][capacity][hd]
+            kc = np.zeros((rows, s.n_kv_heads, capacity, s.head_dim))
+            vc = np.zeros((rows, s.n_kv_heads, capacity, s.head_dim))
+            kc[:, :, :P] = k.transpose(1, 0, 2)[None]
+            vc[:, :, :P] = v.transpose(1, 0, 2)[None]
+            state["k"].append(kc)
+            state["v"].append(vc)
+        out = rmsnorm(h, self.w("final_norm"), s.rms_eps)
+        return state, out[-1] @ self.w("head").T
+
+    @staticmethod
+    def select_rows(state, idx):
+        """Keep only the rows ``idx`` of a decode state."""
+        idx = np.asarray(idx, dtype=np.int64)
+        return {"k": [k[idx] for k in state["k"]], "v": [v[idx] for v in state["v"]],
+                "pos": state["pos"]}
+
+    def step(self, state, tokens):
+        """Append one token per row at position state['pos']; return logits [rows][V]."""
+        s = self.s
+        tokens = np.asarray(tokens, dtype=np.int64)
+        rows = len(tokens)
+        pos = state["pos"]
+        h = widen(self.raw["embed"][tokens])
+        cos, sin = rope_cos_sin(np.array([pos]), s.head_dim, s.rope_theta)
+        scale = 1.0 / np.sqrt(s.head_dim)
+        for l in range(s.n_layers):
+            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)   # [rows][heads][hd]
+            q, k = rope(q, cos, sin), rope(k, cos, sin)
+            state["k"][l][:, :, pos] = k
+            state["v"][l][:, :, pos] = v
+            K = state["k"][l][:, :, :pos + 1]                     # [rows][kvh][T][hd]
+            V = state["v"][l][:, :, :pos + 1]
+            o = np.empty((rows, s.n_heads, s.head_dim))
+            for j in range(s.n_heads):
+                kh = self.kv_head_of(j)
+                sc = np.einsum("rd,rtd->rt", q[:, j, :], K[:, kh]) * scale
+                o[:, j, :] = np.einsum("rt,rtd->rd", softmax(sc), V[:, kh])
+            h = h + o.reshape(rows, -1) @ self.w("wo", l).T
+            h = h + self._ffn(h, l)
+        state["pos"] = pos + 1
+        out = rmsnorm(h, self.w("final_norm"), s.rms_eps)
+        return out @ self.w("head").T
