@@ -1,0 +1,330 @@
+// Projections of the decoder (QKV, O, gate|up + SwiGLU, down, LM head):
+// C[m][n] = sum_k A[m][k] * B[n][k], A = activations [M][lda], B = weights
+// [N][ldb] (both K-contiguous), fp32 accumulation, fused epilogues.
+//
+// bf16: MFMA v_mfma_f32_16x16x32_bf16 tiles staged through LDS with double
+// buffering.  fp32: a plain LDS-tiled FMA kernel (used by the fp32 model).
+// Split-K writes fp32 partials [split][M][Nout] that a second kernel sums in
+// split order, so results do not depend on scheduling.
+#include "common.h"
+#include "kernels.h"
+
+namespace sr {
+
+// ---------------------------------------------------------------- epilogues
+struct EpiArgs {
+  int mode;       // GemmEpi
+  void* out;      // destination (type per mode)
+  int ldo;        // leading dimension of out (elements)
+  int out_bf16;   // for EPI_STORE and EPI_SWIGLU: 1 = bf16 out, 0 = fp32 out
+};
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
+
+__device__ __forceinline__ void store_out(const EpiArgs& e, int m, int n, float v) {
+  if (e.out_bf16)
+    reinterpret_cast<bf16_t*>(e.out)[(int64_t)m * e.ldo + n] = f32_to_bf16(v);
+  else
+    reinterpret_cast<float*>(e.out)[(int64_t)m * e.ldo + n] = v;
+}
+
+// Single-output epilogue (modes EPI_STORE, EPI_RESID).
+__device__ __forceinline__ void epi_one(const EpiArgs& e, int m, int n, float v) {
+  if (e.mode == EPI_RESID) {
+    float* h = reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n;
+    *h = *h + v;
+  } else {
+    store_out(e, m, n, v);
+  }
+}
+
+// ------------------------------------------------------------ bf16 MFMA GEMM
+// Block tile BM x BN (x2 when PAIRED: gate rows n and up rows pair_off + n),
+// K step BK, wave tile WM x WN.  PAIRED epilogue: silu(gate) * up.
+template <int BM, int BN, int BK, int WM, int WN, bool PAIRED>
+__global__ void __launch_bounds__((BM / WM) * (BN / WN) * 64)
+gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                 int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                 float* __restrict__ partial) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  constexpr int NB = PAIRED ? 2 : 1;
+  constexpr int PAD = 8;
+  constexpr int LDS_ROW = BK + PAD;  // bf16 elements per LDS row
+  constexpr int TM = WM / 16, TN = WN / 16;
+  constexpr int CH_ROW = BK / 8;     // 16-byte chunks per row
+  constexpr int A_CH = BM * CH_ROW, B_CH = NB * BN * CH_ROW;
+  constexpr int A_IT = (A_CH + NT - 1) / NT, B_IT = (B_CH + NT - 1) / NT;
+
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDS_ROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][NB * BN * LDS_ROW];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / (BN / WN)) * WM, wn0 = (wave % (BN / WN)) * WN;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int k_begin = blockIdx.z * k_per_split;
+  const int k_end = min(K, k_begin + k_per_split);
+  const int nk = (k_end - k_begin) / BK;
+
+  f32x4 acc[NB][TM][TN];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  uint4 ra[A_IT], rb[B_IT];
+  auto load_global = [&](int kt) {
+    const int kb = k_begin + kt * BK;
+#pragma unroll
+    for (int it = 0; it < A_IT; ++it) {
+      int c = tid + it * NT;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (c < A_CH) {
+        int r = c / CH_ROW, cc = c % CH_ROW;
+        int m = m0 + r;
+        if (m < M) v = *reinterpret_cast<const uint4*>(A + (int64_t)m * lda + kb + cc * 8);
+      }
+      ra[it] = v;
+    }
+#pragma unroll
+    for (int it = 0; it < B_IT; ++it) {
+      int c = tid + it * NT;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (c < B_CH) {
+        int r = c / CH_ROW, cc = c % CH_ROW;
+        int blk = r / BN, rr = r % BN;
+        int n = n0 + rr;
+        if (n < N)
+          v = *reinterpret_cast<const uint4*>(B + blk * pair_off + (int64_t)n * ldb + kb + cc * 8);
+      }
+      rb[it] = v;
+    }
+  };
+  auto store_lds = [&](int buf) {
+#pragma unroll
+    for (int it = 0; it < A_IT; ++it) {
+      int c = tid + it * NT;
+      if (c < A_CH) {
+        int r = c / CH_ROW, cc = c % CH_ROW;
+        *reinterpret_cast<uint4*>(&As[buf][r * LDS_ROW + cc * 8]) = ra[it];
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < B_IT; ++it) {
+      int c = tid + it * NT;
+      if (c < B_CH) {
+        int r = c / CH_ROW, cc = c % CH_ROW;
+        *reinterpret_cast<uint4*>(&Bs[buf][r * LDS_ROW + cc * 8]) = rb[it];
+      }
+    }
+  };
+
+  if (nk > 0) {
+    load_global(0);
+    store_lds(0);
+  }
+  __syncthreads();
+  const int fr = lane & 15, fg = lane >> 4;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_global(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 32) {
+      bf16x8 af[TM];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm0 + i * 16 + fr) * LDS_ROW + ks + fg * 8]);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          bf16x8 bfr = *reinterpret_cast<const bf16x8*>(
+              &Bs[buf][(b * BN + wn0 + j * 16 + fr) * LDS_ROW + ks + fg * 8]);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr, acc[b][i][j], 0, 0, 0);
+        }
+    }
+    if (kt + 1 < nk) store_lds(buf ^ 1);
+    __syncthreads();
+  }
+
+  // Accumulator layout: lane holds rows 4*(lane/16) + e, column lane % 16.
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        int m = m0 + wm0 + i * 16 + fg * 4 + e;
+        int n = n0 + wn0 + j * 16 + fr;
+        if (m >= M || n >= N) continue;
+        if (partial) {
+          const int nout = NB * N;
+          float* p = partial + ((int64_t)blockIdx.z * M + m) * nout;
+          p[n] = acc[0][i][j][e];
+          if (PAIRED) p[N + n] = acc[NB - 1][i][j][e];
+        } else if (PAIRED) {
+          store_out(epi, m, n, silu(acc[0][i][j][e]) * acc[NB - 1][i][j][e]);
+        } else {
+          epi_one(epi, m, n, acc[0][i][j][e]);
+        }
+      }
+}
+
+// ------------------------------------------------------------ fp32 GEMM
+// 64 x 64 block tile, 256 threads, 4 x 4 outputs per thread, K step 16.
+// Always writes to `partial` ([1][M][NB*N]); the reduce kernel applies the
+// epilogue.
+__global__ void __launch_bounds__(256)
+gemm_f32_kernel(const float* __restrict__ A, int lda, const float* __restrict__ B, int ldb,
+                int64_t pair_off, int paired, int M, int N, int K, float* __restrict__ partial) {
+  __shared__ float As[16][64 + 1];
+  __shared__ float Bs[16][64 + 1];
+  const int tid = threadIdx.x;
+  const int tx = tid % 16, ty = tid / 16;
+  const int m0 = blockIdx.y * 64;
+  const int nb = paired ? 2 : 1;
+  const int ncols = nb * N;
+  const int n0 = blockIdx.x * 64;  // over the concatenated [gate | up] columns
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    for (int c = tid; c < 64 * 16; c += 256) {
+      int r = c / 16, kk = c % 16;
+      int m = m0 + r, n = n0 + r;
+      As[kk][r] = (m < M) ? A[(int64_t)m * lda + k0 + kk] : 0.f;
+      float bv = 0.f;
+      if (n < ncols) {
+        int blk = n / N, nn = n % N;
+        bv = B[blk * pair_off + (int64_t)nn * ldb + k0 + kk];
+      }
+      Bs[kk][r] = bv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+      if (m < M && n < ncols) partial[(int64_t)m * ncols + n] = acc[i][j];
+    }
+}
+
+// Sum split-K partials in split order, then apply the epilogue.
+__global__ void gemm_reduce_kernel(const float* __restrict__ partial, int splits, int M, int N,
+                                   int paired, EpiArgs epi) {
+  const int nout = paired ? 2 * N : N;
+  const int64_t total = (int64_t)M * N;
+  for (int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * blockDim.x) {
+    int m = (int)(idx / N), n = (int)(idx % N);
+    float g = 0.f, u = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      const float* p = partial + ((int64_t)s * M + m) * nout;
+      g += p[n];
+      if (paired) u += p[N + n];
+    }
+    if (paired)
+      store_out(epi, m, n, silu(g) * u);
+    else
+      epi_one(epi, m, n, g);
+  }
+}
+
+// ------------------------------------------------------------ dispatch
+template <int BM, int BN, int BK, int WM, int WN, bool PAIRED>
+static void launch_bf16(const GemmArgs& g, int splits, int kps, const EpiArgs& e, float* part,
+                        hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, splits);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WM, WN, PAIRED>), grid, dim3(NT), 0, s,
+                     (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N,
+                     g.K, kps, e, part);
+  SR_CHECK_LAUNCH();
+}
+
+size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired) {
+  GemmPlan p = gemm_plan(dtype, M, N, K, paired);
+  if (p.splits <= 1 && dtype == SR_BF16) return 0;
+  return (size_t)p.splits * M * (paired ? 2 * (size_t)N : (size_t)N);
+}
+
+GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
+  GemmPlan p;
+  p.splits = 1;
+  if (dtype != SR_BF16) return p;
+  int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
+  int bn = paired ? 64 : 128;
+  int64_t tiles = (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  // Split K when the tile grid alone cannot fill 256 CUs twice over; each
+  // split keeps at least 512 of K and a multiple of 64.
+  int splits = 1;
+  while (tiles * splits < 512 && K % (splits * 2 * 64) == 0 && K / (splits * 2) >= 512 && splits < 8)
+    splits *= 2;
+  p.splits = splits;
+  return p;
+}
+
+void gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
+  SR_REQUIRE(g.K % 64 == 0, 3, "GEMM K must be a multiple of 64");
+  EpiArgs e{g.epi, g.out, g.ldo, g.out_bf16};
+  if (g.M == 0 || g.N == 0) return;
+  if (g.dtype == SR_F32) {
+    const int ncols = (g.paired ? 2 : 1) * g.N;
+    SR_REQUIRE((size_t)g.M * ncols <= partial_cap, 5, "GEMM partial buffer too small");
+    dim3 grid((ncols + 63) / 64, (g.M + 63) / 64);
+    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, (const float*)g.A, g.lda,
+                       (const float*)g.B, g.ldb, g.pair_off, (int)g.paired, g.M, g.N, g.K, partial);
+    SR_CHECK_LAUNCH();
+    int64_t total = (int64_t)g.M * g.N;
+    int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, partial, 1, g.M, g.N,
+                       (int)g.paired, e);
+    SR_CHECK_LAUNCH();
+    return;
+  }
+  GemmPlan plan = gemm_plan(g.dtype, g.M, g.N, g.K, g.paired);
+  const int splits = plan.splits;
+  const int kps = g.K / splits;
+  SR_REQUIRE(kps * splits == g.K && kps % 64 == 0, 5, "split-K must divide K into multiples of 64");
+  float* part = nullptr;
+  if (splits > 1) {
+    SR_REQUIRE((size_t)splits * g.M * (g.paired ? 2 : 1) * (size_t)g.N <= partial_cap, 5,
+               "GEMM partial buffer too small");
+    part = partial;
+  }
+  if (g.paired) {
+    if (g.M <= 32) launch_bf16<32, 64, 64, 32, 16, true>(g, splits, kps, e, part, s);
+    else if (g.M <= 64) launch_bf16<64, 64, 64, 32, 32, true>(g, splits, kps, e, part, s);
+    else launch_bf16<128, 64, 64, 64, 32, true>(g, splits, kps, e, part, s);
+  } else {
+    if (g.M <= 32) launch_bf16<32, 128, 64, 32, 32, false>(g, splits, kps, e, part, s);
+    else if (g.M <= 64) launch_bf16<64, 128, 64, 32, 64, false>(g, splits, kps, e, part, s);
+    else launch_bf16<128, 128, 64, 64, 64, false>(g, splits, kps, e, part, s);
+  }
+  if (splits > 1) {
+    int64_t total = (int64_t)g.M * g.N;
+    int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, g.M, g.N,
+                       (int)g.paired, e);
+    SR_CHECK_LAUNCH();
+  }
+}
+
+}  // namespace sr

@@ -1,0 +1,120 @@
+"""End-to-end parity of sr_generate against the oracle.
+
+fp32 tiny configuration: the oracle runs the whole algorithm independently;
+the GPU must return the same candidate, tokens, rounds and survivors, with
+rewards within 1e-4 max|x|.  bf16 configurations: the GPU drives and the
+oracle audits its trace -- the cut on the GPU's scores, the sampler on the
+GPU's logits, the answer on the GPU's final rewards (all bit-exact), and
+teacher-forced logits and rewards on the GPU's sequences (within 2e-2 max|x|).
+"""
+import numpy as np
+import pytest
+
+from gpu_util import device_models, host_models, need_gpu, oracle_models, say, tol
+from oracle import sampler as osamp
+from oracle import specrej
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_run(name, **over):
+    torch, sr = need_gpu()
+    c, gen, rm, prompt = device_models(name)
+    c = c.with_(**over)
+    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id, c.max_rounds)
+    out = sr.generate(gen, rm, prompt, p, trace=True)
+    return c, prompt, out
+
+
+def trace_rounds(out):
+    t = out["trace"]
+    rounds = []
+    for r in range(t["rounds"]):
+        b = int(t["round_b"][r])
+        cand = t["round_cand"][r, :b].tolist()
+        rounds.append((int(t["round_L"][r]), b, int(t["round_keep"][r]), cand,
+                       t["round_scores"][r, :b].copy(), t["round_accept"][r, :b].copy()))
+    return rounds
+
+
+def check_trace_logic(c, out):
+    """What must hold of any run, whatever the model numerics."""
+    t = out["trace"]
+    rounds = trace_rounds(out)
+    for (L, b, K, cand, scores, acc) in rounds:
+        assert K == specrej.keep_count(b, c.alpha)
+        assert cand == sorted(cand)
+        sd = {k: float(s) for k, s in zip(cand, scores)}
+        kept = set(specrej.top_k(cand, sd, K))
+        assert [int(a) for a in acc] == [1 if k in kept else 0 for k in cand]
+    fs = t["final_scores"]
+    members = {k: float(fs[k]) for k in range(c.n) if not np.isnan(fs[k])}
+    assert out["best_index"] == specrej.arg_best(members)
+    assert out["best_score"] == np.float32(members[out["best_index"]])
+    lens = t["all_len"]
+    assert out["generated_tokens"] == int(lens.sum())
+    assert out["tokens"] == t["all_tokens"][out["best_index"], : lens[out["best_index"]]].tolist()
+    return rounds
+
+
+@pytest.mark.parametrize("over", [{}, {"eos_id": 2}, {"max_rounds": 1}, {"alpha": 0.0},
+                                  {"n": 40, "alpha": 0.1, "tau": 4, "max_new_tokens": 24}])
+def test_tiny_fp32_matches_full_oracle(over):
+    say(f"tiny_fp32 e2e {over}")
+    c, prompt, out = gpu_run("tiny_fp32", **over)
+    rounds = check_trace_logic(c, out)
+    g, rm = oracle_models("tiny_fp32")
+    ref = specrej.speculative_rejection(g, rm, prompt, c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature,
+                                        c.sample_seed, c.eos_id, c.max_rounds)
+    t = out["trace"]
+    # every candidate's tokens
+    for k in range(c.n):
+        assert t["all_tokens"][k, : t["all_len"][k]].tolist() == ref["responses"][k], k
+    assert [(L, b, K) for (L, b, K, *_rest) in rounds] == [r[:3] for r in ref["rounds"]]
+    for (L, b, K, cand, scores, acc), (rL, rb, rK, racc, rsc) in zip(rounds, ref["rounds"]):
+        assert cand == sorted(rsc)
+        want = np.array([rsc[k] for k in cand])
+        assert np.abs(scores - want).max() <= 1e-4 * np.abs(want).max()
+        assert sorted(k for k, a in zip(cand, acc) if a) == sorted(racc)
+    assert out["best_index"] == ref["best"] and out["tokens"] == ref["tokens"]
+    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * max(1.0, abs(ref["score"]))
+    assert out["generated_tokens"] == ref["generated"]
+    if c.eos_id < 0:
+        assert out["generated_tokens"] == specrej.schedule(c.n, c.alpha, c.tau, c.max_new_tokens, c.max_rounds)[1]
+
+
+@pytest.mark.parametrize("name", ["small_bf16"])
+def test_bf16_audit(name):
+    torch, sr = need_gpu()
+    say(f"{name} e2e audit")
+    c, prompt, out = gpu_run(name)
+    rounds = check_trace_logic(c, out)
+    sched, total = specrej.schedule(c.n, c.alpha, c.tau, c.max_new_tokens)
+    assert [(L, b, K) for (L, b, K, *_rest) in rounds] == sched
+    assert out["generated_tokens"] == total
+    t = out["trace"]
+    _, gen, rm, _ = device_models(name)
+    g, orm = oracle_models(name)
+    # (1) the sampler on the GPU's own first-round logits reproduces its tokens
+    toks = t["all_tokens"][:, : c.tau].astype(np.int32)
+    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    lg = sr.logits_teacher_forced(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), ws).cpu().numpy()
+    for k in range(c.n):
+        for step in range(c.tau):
+            assert osamp.sample(lg[k, step], c.temperature, c.sample_seed, k, step) == toks[k, step], (k, step)
+    # (2) those logits match the float64 oracle on the same sequences
+    for k in (0, c.n // 2, c.n - 1):
+        ref = g.logits(list(prompt) + list(toks[k]))[len(prompt) - 1: len(prompt) - 1 + c.tau]
+        assert np.abs(lg[k] - ref).max() <= tol(c) * np.abs(ref).max()
+    # (3) partial rewards of the first cut, recomputed by the oracle
+    L0, b0, K0, cand0, sc0, acc0 = rounds[0]
+    for j in (0, 7, b0 - 1):
+        k = cand0[j]
+        ref = orm.score(list(prompt) + t["all_tokens"][k, :L0].tolist())
+        assert abs(sc0[j] - ref) <= tol(c) * max(abs(ref), np.abs(sc0).max())
+    # (4) final rewards of I, recomputed by the oracle
+    fs = t["final_scores"]
+    mem = [k for k in range(c.n) if not np.isnan(fs[k])]
+    refs = np.array([orm.score(list(prompt) + t["all_tokens"][k, : t["all_len"][k]].tolist()) for k in mem])
+    assert np.abs(fs[mem] - refs).max() <= tol(c) * np.abs(refs).max()
