@@ -1,0 +1,210 @@
+"""Benchmark of the Speculative Rejection hot path on one MI355X.
+
+One step = one sr_generate call: the whole hot path (prompt prefill of both
+models, batched decode of N candidates, reward-model scoring at every
+decision token, the rejection cuts and KV compaction, the final arg max) for
+one prompt.  Default workload: the 8B-shaped generator and reward model
+(32 layers, d=4096, 32/8 heads, hd=128, ffn 14336, vocab 128256; bf16,
+random N(0, 0.02) weights), a 256-token random prompt, N=512, tau=128,
+alpha=0.8, 1024 new tokens, temperature 1, no EOS.
+
+Reports generator tokens/s (sampled response tokens / seconds per prompt),
+seconds per prompt, the same for alpha=0 (Best-of-N at equal N) and the
+speedup, the roofline of the dominant kernel class measured with HIP events
+during the timed steps, and the CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "generator tokens/s and s/prompt at N, α (vs α=0 Best-of-N); % HBM/MFMA peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+FP32_VECTOR_TFLOPS = 157.3
+# kernel class -> (bound, unit) for the implementation in this library
+BOUNDS = {
+    "gen_gemm_mfma": ("mfma", "TFLOP/s"), "gen_gemm_hbm": ("hbm", "GB/s"), "decode_attn": ("hbm", "GB/s"),
+    "rm_gemm": ("mfma", "TFLOP/s"), "prefill_attn": ("alu", "TFLOP/s"), "sample": ("hbm", "GB/s"),
+    "cut": ("hbm", "GB/s"), "other": ("hbm", "GB/s"),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def roofline_of(name, k, dtype):
+    bound, unit = BOUNDS[name]
+    if k["sec"] <= 0:
+        return None
+    if unit == "GB/s":
+        achieved, peak = k["bytes"] / k["sec"] / 1e9, PEAK_HBM_GBS
+    else:
+        achieved = k["flops"] / k["sec"] / 1e12
+        peak = FP32_VECTOR_TFLOPS if bound == "alu" else PEAK_TFLOPS[dtype]
+    return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "avg_launch_us": round(k["sec"] / max(1, k["launches"]) * 1e6, 2), "launches_timed": k["launches"]}
+
+
+def cpu_baseline(cfg, gw, rows, steps, prompt_len):
+    """The oracle's batched decode on the same generator, bounded sample."""
+    import numpy as np
+
+    from oracle.sampler import sample
+    from oracle.transformer import Transformer
+
+    g = Transformer(cfg.model, gw, False, cache_f64=True)
+    prompt = list(range(1, prompt_len + 1))
+    state, l0 = g.start(prompt, rows, prompt_len + steps + 1)   # widens weights (not timed)
+    toks = [sample(np.float32(l0), 1.0, 42, k, 0) for k in range(rows)]
+    t0 = time.perf_counter()
+    for s in range(1, steps + 1):
+        lg = g.step(state, toks)
+        toks = [sample(np.float32(lg[k]), 1.0, 42, k, s) for k in range(rows)]
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
+    except Exception:
+        cores = os.cpu_count()
+    return {"value": round(rows * steps / dt, 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"oracle float64 decode of {rows} candidates x {steps} steps on the same generator "
+                      f"(prompt prefix of {prompt_len} tokens, weights widened beforehand, untimed); "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="8b_bf16")
+    ap.add_argument("--alpha", type=float, default=None)
+    ap.add_argument("--tau", type=int, default=None)
+    ap.add_argument("--profile-every", type=int, default=16)
+    ap.add_argument("--no-bon", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=8)
+    ap.add_argument("--cpu-steps", type=int, default=6)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the hot path is one GPU's batch of "
+              "candidates; see the design notes for how it would shard", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2410_20290_amd as sr
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = synth.CONFIGS[args.config]
+    if args.alpha is not None:
+        cfg = cfg.with_(alpha=args.alpha)
+    if args.tau is not None:
+        cfg = cfg.with_(tau=args.tau)
+    m = cfg.model
+    t = time.time()
+    gw = synth.model_weights(m, cfg.gen_seed, False)
+    rw = synth.model_weights(m, cfg.rm_seed, True)
+    prompt = synth.prompt(cfg)
+    log(f"[bench] weights generated in {time.time() - t:.1f}s")
+    gen = sr.DeviceModel.upload(m, gw, False)
+    rm = sr.DeviceModel.upload(m, rw, True)
+    del rw
+    torch.cuda.synchronize()
+    log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
+
+    p = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
+                       cfg.eos_id, 0, 0)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    log(f"[bench] workspace {ws.nbytes / 2**30:.2f} GiB")
+    for i in range(args.warmup):
+        o = sr.generate(gen, rm, prompt, p, ws)
+        log(f"[bench] warmup {i}: {o['sec_total']:.3f}s generated={o['generated_tokens']}")
+    pp = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
+                        cfg.eos_id, 0, args.profile_every)
+    kern = {}
+    gen_tokens = 0
+    results = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        o = sr.generate(gen, rm, prompt, pp, ws)
+        results.append(o)
+        gen_tokens += o["generated_tokens"]
+        for name, k in o["kernels"].items():
+            a = kern.setdefault(name, {"sec": 0.0, "launches": 0, "bytes": 0.0, "flops": 0.0})
+            for f in a:
+                a[f] += k[f]
+        log(f"[bench] step {i}: {o['sec_total']:.3f}s (prefill {o['sec_prefill']:.3f} decode {o['sec_decode']:.3f} "
+            f"reward {o['sec_reward']:.3f} cut {o['sec_cut']:.3f}) best={o['best_index']} rounds={o['rounds']}")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    s_per_prompt = elapsed / args.steps
+    value = gen_tokens / elapsed
+    del ws
+    torch.cuda.empty_cache()
+
+    bon = None
+    if not args.no_bon and cfg.alpha > 0:
+        pb = sr.make_params(cfg.n, 0.0, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
+                            cfg.eos_id, 0, 0)
+        wsb = sr.Workspace(gen, rm, len(prompt), pb)
+        torch.cuda.synchronize()
+        tb = time.perf_counter()
+        ob = sr.generate(gen, rm, prompt, pb, wsb)
+        torch.cuda.synchronize()
+        tb = time.perf_counter() - tb
+        bon = {"s_per_prompt": round(tb, 4), "tokens_per_s": round(ob["generated_tokens"] / tb, 1),
+               "generated_tokens": ob["generated_tokens"], "best_index": ob["best_index"],
+               "sr_best_index": results[-1]["best_index"]}
+        log(f"[bench] best-of-N (alpha=0): {tb:.3f}s")
+        del wsb
+        torch.cuda.empty_cache()
+
+    kernels = {}
+    for name, k in kern.items():
+        r = roofline_of(name, k, m.dtype)
+        if r:
+            r["sec_timed"] = round(k["sec"], 4)
+            kernels[name] = r
+    dominant = max(kern, key=lambda n: kern[n]["sec"])
+    roof = dict(kernels[dominant])
+
+    cpu = None
+    if not args.no_cpu:
+        del gen, rm
+        torch.cuda.empty_cache()
+        log("[bench] timing the CPU oracle sample")
+        cpu = cpu_baseline(cfg, gw, args.cpu_rows, args.cpu_steps, 16)
+
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(s_per_prompt * 1e3, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": m.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: 8B-shaped bf16 generator + reward model, prompt {cfg.prompt_len}, "
+                               f"N={cfg.n}, tau={cfg.tau}, alpha={cfg.alpha}, {cfg.max_new_tokens} new tokens",
+                   "N": cfg.n, "alpha": cfg.alpha, "tau": cfg.tau, "max_new_tokens": cfg.max_new_tokens,
+                   "prompt_len": cfg.prompt_len},
+        "s_per_prompt": round(s_per_prompt, 4),
+        "generated_tokens_per_prompt": results[-1]["generated_tokens"],
+        "phases_s": {k: round(results[-1][k], 4) for k in ("sec_prefill", "sec_decode", "sec_reward", "sec_cut")},
+        "best_of_n": bon,
+        "speedup_vs_alpha0": round(bon["s_per_prompt"] / s_per_prompt, 3) if bon else None,
+        "roofline": roof,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

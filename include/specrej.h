@@ -100,7 +100,11 @@ typedef struct {
  *               at step t is word 0 of Philox(counter (t, k, 0, 0),
  *               key (seed mod 2^32, seed div 2^32)).
  *  eos_id       end-of-sequence token (part of the response), -1 = none.
- *  max_rounds   maximum number of cuts, 0 = unlimited. */
+ *  max_rounds   maximum number of cuts, 0 = unlimited.
+ *  profile_every  0 = off; k > 0 = time kernels with HIP events on `stream`
+ *               during every k-th decode step and every reward/cut phase,
+ *               accumulating into sr_result.kernel_* (costs one host
+ *               synchronisation per timed step). */
 typedef struct {
   int32_t n;
   double alpha;
@@ -109,8 +113,26 @@ typedef struct {
   uint64_t seed;
   int32_t eos_id;
   int32_t max_rounds;
+  int32_t profile_every;
 } sr_params;
 
+/* Kernel classes of sr_result.kernel_*. */
+enum {
+  SR_K_GEN_GEMM_MFMA = 0,   /* generator projections with >= 312 rows (MFMA-bound)  */
+  SR_K_GEN_GEMM_HBM = 1,    /* generator projections with < 312 rows (weight-bound) */
+  SR_K_DECODE_ATTN = 2,     /* decode attention (+ split merge)                      */
+  SR_K_RM_GEMM = 3,         /* reward-model and prompt-prefill projections           */
+  SR_K_PREFILL_ATTN = 4,    /* prefill attention                                     */
+  SR_K_SAMPLE = 5,          /* sampler + state update                                */
+  SR_K_CUT = 6,             /* cut, compaction, arg max                              */
+  SR_K_OTHER = 7,           /* embedding, RMSNorm, RoPE, reward head, gathers        */
+  SR_K_NCLASS = 8
+};
+
+/* kernel_sec/launches/bytes/flops: per kernel class, the event-measured time,
+ * the number of timed launches and their algorithmic HBM bytes and flops
+ * (the bytes and flops the operation itself must move or compute: every
+ * weight, activation and KV element once).  Zero unless profile_every > 0. */
 typedef struct {
   int32_t best_index;        /* candidate index k* (eq. output)              */
   float best_score;          /* s(x, y_k*)                                   */
@@ -118,6 +140,10 @@ typedef struct {
   int32_t rounds;            /* number of cuts performed                     */
   int64_t generated_tokens;  /* response tokens sampled over all candidates  */
   double sec_total, sec_prefill, sec_decode, sec_reward, sec_cut;
+  double kernel_sec[SR_K_NCLASS];
+  int64_t kernel_launches[SR_K_NCLASS];
+  double kernel_bytes[SR_K_NCLASS];
+  double kernel_flops[SR_K_NCLASS];
 } sr_result;
 
 /* Optional host buffers filled by sr_generate for tests and tracing; any

@@ -40,15 +40,23 @@ class sr_model(ctypes.Structure):
     _fields_ = [("cfg", sr_model_config), ("w", sr_weights)]
 
 
+NCLASS = 8
+KERNEL_CLASSES = ["gen_gemm_mfma", "gen_gemm_hbm", "decode_attn", "rm_gemm", "prefill_attn", "sample", "cut",
+                  "other"]
+
+
 class sr_params(ctypes.Structure):
     _fields_ = [("n", _i32), ("alpha", _f64), ("tau", _i32), ("max_new_tokens", _i32),
-                ("temperature", _f32), ("seed", _u64), ("eos_id", _i32), ("max_rounds", _i32)]
+                ("temperature", _f32), ("seed", _u64), ("eos_id", _i32), ("max_rounds", _i32),
+                ("profile_every", _i32)]
 
 
 class sr_result(ctypes.Structure):
     _fields_ = [("best_index", _i32), ("best_score", _f32), ("n_tokens", _i32), ("rounds", _i32),
                 ("generated_tokens", _i64), ("sec_total", _f64), ("sec_prefill", _f64),
-                ("sec_decode", _f64), ("sec_reward", _f64), ("sec_cut", _f64)]
+                ("sec_decode", _f64), ("sec_reward", _f64), ("sec_cut", _f64),
+                ("kernel_sec", _f64 * NCLASS), ("kernel_launches", _i64 * NCLASS),
+                ("kernel_bytes", _f64 * NCLASS), ("kernel_flops", _f64 * NCLASS)]
 
 
 class sr_trace(ctypes.Structure):
@@ -148,8 +156,9 @@ class DeviceModel:
         return DeviceModel(shape, reward, ts, sr_model(cfg, w))
 
 
-def make_params(n, alpha, tau, max_new_tokens, temperature=1.0, seed=42, eos_id=-1, max_rounds=0) -> sr_params:
-    return sr_params(n, alpha, tau, max_new_tokens, temperature, seed, eos_id, max_rounds)
+def make_params(n, alpha, tau, max_new_tokens, temperature=1.0, seed=42, eos_id=-1, max_rounds=0,
+                profile_every=0) -> sr_params:
+    return sr_params(n, alpha, tau, max_new_tokens, temperature, seed, eos_id, max_rounds, profile_every)
 
 
 def workspace_size(gen: DeviceModel, rm: DeviceModel, prompt_len: int, p: sr_params) -> int:
@@ -196,7 +205,10 @@ def generate(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, ws: Worksp
                            ctypes.byref(p), ws.ptr, ws.nbytes, _stream(stream), out_tokens.ctypes.data,
                            ctypes.byref(res), ctypes.byref(tr) if tr is not None else None)
     _check(st)
-    out = {f: getattr(res, f) for f, _ in sr_result._fields_}
+    out = {f: getattr(res, f) for f, _ in sr_result._fields_ if not f.startswith("kernel_")}
+    out["kernels"] = {name: {"sec": res.kernel_sec[i], "launches": int(res.kernel_launches[i]),
+                             "bytes": res.kernel_bytes[i], "flops": res.kernel_flops[i]}
+                      for i, name in enumerate(KERNEL_CLASSES)}
     out["tokens"] = out_tokens[:res.n_tokens].tolist()
     if trace:
         R = res.rounds

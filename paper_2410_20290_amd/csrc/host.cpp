@@ -10,6 +10,7 @@
 // packed into the other pool for the next round.  The host synchronises
 // with the device once per round (to learn the survivor count).
 #include <algorithm>
+#include <functional>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -262,30 +263,102 @@ struct Model {
   const void* w2(int l) const { return wb(w->w2, (int64_t)l * m.d * m.ff); }
 };
 
+// Optional per-kernel-class timing with HIP events on the caller's stream.
+struct Profiler {
+  hipStream_t s = nullptr;
+  bool active = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  struct Rec {
+    int cls;
+    size_t e0, e1;
+    double bytes, flops;
+  };
+  std::vector<Rec> recs;
+  double sec[SR_K_NCLASS] = {}, bytes[SR_K_NCLASS] = {}, flops[SR_K_NCLASS] = {};
+  int64_t n[SR_K_NCLASS] = {};
+  ~Profiler() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+  size_t mark() {
+    if (used == pool.size()) {
+      hipEvent_t e;
+      SR_HIP(hipEventCreate(&e));
+      pool.push_back(e);
+    }
+    SR_HIP(hipEventRecord(pool[used], s));
+    return used++;
+  }
+  // Waits for the recorded launches and accumulates their durations.
+  void flush() {
+    if (!recs.empty()) {
+      SR_HIP(hipEventSynchronize(pool[recs.back().e1]));
+      for (const Rec& r : recs) {
+        float ms = 0.f;
+        SR_HIP(hipEventElapsedTime(&ms, pool[r.e0], pool[r.e1]));
+        sec[r.cls] += ms * 1e-3;
+        bytes[r.cls] += r.bytes;
+        flops[r.cls] += r.flops;
+        n[r.cls] += 1;
+      }
+      recs.clear();
+    }
+    used = 0;
+  }
+};
+
 struct Ctx {
   const Plan* pl;
   Layout* L;
   hipStream_t s;
+  Profiler* prof;
 };
 
-static void run_gemm(const Ctx& c, int dtype, const void* A, int lda, const void* B, int ldb, int M,
-                     int N, int K, int epi, void* out, int ldo, int out_bf16, bool paired = false,
+template <typename F>
+static void timed(const Ctx& c, int cls, double bytes, double flops, F&& launch) {
+  Profiler* p = c.prof;
+  if (!p || !p->active) {
+    launch();
+    return;
+  }
+  const size_t a = p->mark();
+  launch();
+  const size_t b = p->mark();
+  p->recs.push_back({cls, a, b, bytes, flops});
+}
+
+// Projection launch.  decode: a generator decode projection (classed by
+// whether its rows make it MFMA- or weight-bound), else reward/prefill.
+static void run_gemm(const Ctx& c, bool decode, int dtype, const void* A, int lda, const void* B, int ldb,
+                     int M, int N, int K, int epi, void* out, int ldo, int out_bf16, bool paired = false,
                      int64_t pair_off = 0) {
   GemmArgs g;
   g.dtype = dtype; g.A = A; g.lda = lda; g.B = B; g.ldb = ldb; g.pair_off = pair_off;
   g.paired = paired; g.M = M; g.N = N; g.K = K; g.epi = epi; g.out = out; g.ldo = ldo;
   g.out_bf16 = out_bf16;
-  gemm(g, c.L->gpart, c.pl->gpart, c.s);
+  const double es = dtype == SR_BF16 ? 2.0 : 4.0;
+  const double nw = paired ? 2.0 * N : (double)N;
+  double ob = epi == EPI_RESID ? 8.0 : (paired || out_bf16 ? es : 4.0);
+  const double bytes = es * ((double)M * K + nw * K) + ob * (double)M * N;
+  const double flops = 2.0 * M * nw * K;
+  const int cls = decode ? (M >= 312 ? SR_K_GEN_GEMM_MFMA : SR_K_GEN_GEMM_HBM) : SR_K_RM_GEMM;
+  timed(c, cls, bytes, flops, [&] { gemm(g, c.L->gpart, c.pl->gpart, c.s); });
+}
+
+static void run_other(const Ctx& c, double bytes, std::function<void()> f) {
+  timed(c, SR_K_OTHER, bytes, 0.0, f);
 }
 
 // Feed-forward half of a layer: h += W2 (silu(W1 f) * (W3 f)), f = RMSNorm(h).
-static void ffn_block(const Ctx& c, const Model& M, int l, float* h, void* xn, void* u, int rows) {
+static void ffn_block(const Ctx& c, bool decode, const Model& M, int l, float* h, void* xn, void* u,
+                      int rows) {
   const Dims& m = M.m;
   const int bf = m.dtype == SR_BF16;
-  rmsnorm(m.dtype, h, m.d, M.ffn_norm(l), m.d, m.eps, rows, xn, m.d, c.s);
-  run_gemm(c, m.dtype, xn, m.d, M.w13(l), m.d, rows, m.ff, m.d, EPI_STORE, u, m.ff, bf, true,
+  run_other(c, (double)rows * m.d * (4 + m.es),
+            [&] { rmsnorm(m.dtype, h, m.d, M.ffn_norm(l), m.d, m.eps, rows, xn, m.d, c.s); });
+  run_gemm(c, decode, m.dtype, xn, m.d, M.w13(l), m.d, rows, m.ff, m.d, EPI_STORE, u, m.ff, bf, true,
            (int64_t)m.ff * m.d);
-  run_gemm(c, m.dtype, u, m.ff, M.w2(l), m.ff, rows, m.d, m.ff, EPI_RESID, h, m.d, 0);
+  run_gemm(c, decode, m.dtype, u, m.ff, M.w2(l), m.ff, rows, m.d, m.ff, EPI_RESID, h, m.d, 0);
 }
 
 // Prefill of `rows` sequences of `lr` tokens (device tokens [rows][lr]) at
@@ -297,14 +370,16 @@ static void prefill(const Ctx& c, const Model& M, const float2* rope, const int3
   const Dims& m = M.m;
   Layout& L = *c.L;
   const int T = rows * lr;
-  const int bf = m.dtype == SR_BF16;
-  embed(m.dtype, M.w->embed, m.d, tokens, T, L.ch, c.s);
+  run_other(c, (double)T * m.d * (4 + m.es), [&] { embed(m.dtype, M.w->embed, m.d, tokens, T, L.ch, c.s); });
   for (int l = 0; l < m.nl; ++l) {
     void *kd, *vd;
     kv_out(l, &kd, &vd);
-    rmsnorm(m.dtype, L.ch, m.d, M.attn_norm(l), m.d, m.eps, T, L.cxn, m.d, c.s);
-    run_gemm(c, m.dtype, L.cxn, m.d, M.wqkv(l), m.d, T, m.qkv, m.d, EPI_STORE, L.cqkv, m.qkv, 0);
-    rope_scatter(m.dtype, L.cqkv, rows, lr, m.hq, m.hkv, m.hd, rope, pos0, L.cq, kd, vd, lr, 0, c.s);
+    run_other(c, (double)T * m.d * (4 + m.es),
+              [&] { rmsnorm(m.dtype, L.ch, m.d, M.attn_norm(l), m.d, m.eps, T, L.cxn, m.d, c.s); });
+    run_gemm(c, false, m.dtype, L.cxn, m.d, M.wqkv(l), m.d, T, m.qkv, m.d, EPI_STORE, L.cqkv, m.qkv, 0);
+    run_other(c, (double)T * (m.qkv * 4.0 + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
+      rope_scatter(m.dtype, L.cqkv, rows, lr, m.hq, m.hkv, m.hd, rope, pos0, L.cq, kd, vd, lr, 0, c.s);
+    });
     PrefillAttnArgs a;
     a.dtype = m.dtype; a.hd = m.hd; a.hq = m.hq; a.hkv = m.hkv; a.rows = rows; a.lr = lr;
     a.q = L.cq;
@@ -313,12 +388,14 @@ static void prefill(const Ctx& c, const Model& M, const float2* rope, const int3
     a.vpre = pre ? (const char*)pre + l * lay + lay / 2 : nullptr;
     a.P = pre ? P : 0;
     a.kown = kd; a.vown = vd; a.out = L.co;
-    prefill_attn(a, c.s);
-    run_gemm(c, m.dtype, L.co, m.hq * m.hd, M.wo(l), m.hq * m.hd, T, m.d, m.hq * m.hd, EPI_RESID,
+    const double Pp = a.P;
+    const double abytes = 2.0 * m.hkv * m.hd * m.es * (Pp + (double)T) + (double)T * m.hq * m.hd * (4 + m.es);
+    const double aflops = 4.0 * m.hq * m.hd * rows * (Pp * lr + 0.5 * lr * (lr + 1.0));
+    timed(c, SR_K_PREFILL_ATTN, abytes, aflops, [&] { prefill_attn(a, c.s); });
+    run_gemm(c, false, m.dtype, L.co, m.hq * m.hd, M.wo(l), m.hq * m.hd, T, m.d, m.hq * m.hd, EPI_RESID,
              L.ch, m.d, 0);
-    ffn_block(c, M, l, L.ch, L.cxn, L.cu, T);
+    ffn_block(c, false, M, l, L.ch, L.cxn, L.cu, T);
   }
-  (void)bf;
 }
 
 // Prompt prefill of one model into its prefix buffer [nl][2][hkv][P][hd].
@@ -340,13 +417,14 @@ static void reward_rows(const Ctx& c, const Model& R, const int32_t* cand, const
   const int per = std::max(1, pl.Tc / lr);
   for (int r0 = 0; r0 < rows; r0 += per) {
     const int rc = std::min(per, rows - r0);
-    gather_tokens(L.store, pl.Lmax, cand + r0, len + r0, rc, lr, L.ctok, c.s);
+    run_other(c, (double)rc * lr * 8, [&] { gather_tokens(L.store, pl.Lmax, cand + r0, len + r0, rc, lr, L.ctok, c.s); });
     prefill(c, R, L.rope_r, L.ctok, rc, lr, pl.P, L.rpre, pl.P, [&](int, void** k, void** v) {
       *k = L.ck;
       *v = L.cv;
     });
-    score_head(R.m.dtype, L.ch, R.m.d, lr, len + r0, rc, R.w->final_norm, R.w->head, R.m.eps,
-               score + r0, c.s);
+    run_other(c, (double)rc * R.m.d * 4, [&] {
+      score_head(R.m.dtype, L.ch, R.m.d, lr, len + r0, rc, R.w->final_norm, R.w->head, R.m.eps, score + r0, c.s);
+    });
   }
 }
 
@@ -358,30 +436,35 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
   const Dims& m = G.m;
   Layout& L = *c.L;
   const Plan& pl = *c.pl;
-  const int bf = m.dtype == SR_BF16;
-  embed(m.dtype, G.w->embed, m.d, st.tok, rows, L.h, c.s);
+  run_other(c, (double)rows * m.d * (4 + m.es), [&] { embed(m.dtype, G.w->embed, m.d, st.tok, rows, L.h, c.s); });
   const size_t pre_lay = (size_t)2 * m.hkv * pl.P * m.hd * m.es;
   for (int l = 0; l < m.nl; ++l) {
     char* kpool = (char*)pool + (size_t)(2 * l) * pool_block * m.es;
     char* vpool = (char*)pool + (size_t)(2 * l + 1) * pool_block * m.es;
-    rmsnorm(m.dtype, L.h, m.d, G.attn_norm(l), m.d, m.eps, rows, L.xn, m.d, c.s);
-    run_gemm(c, m.dtype, L.xn, m.d, G.wqkv(l), m.d, rows, m.qkv, m.d, EPI_STORE, L.qkv, m.qkv, 0);
-    rope_scatter(m.dtype, L.qkv, rows, 1, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool,
-                 vpool, cap, step - 1, c.s);
+    run_other(c, (double)rows * m.d * (4 + m.es),
+              [&] { rmsnorm(m.dtype, L.h, m.d, G.attn_norm(l), m.d, m.eps, rows, L.xn, m.d, c.s); });
+    run_gemm(c, true, m.dtype, L.xn, m.d, G.wqkv(l), m.d, rows, m.qkv, m.d, EPI_STORE, L.qkv, m.qkv, 0);
+    run_other(c, (double)rows * (m.qkv * 4.0 + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
+      rope_scatter(m.dtype, L.qkv, rows, 1, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool, vpool, cap,
+                   step - 1, c.s);
+    });
     DecodeAttnArgs a;
     a.dtype = m.dtype; a.hd = m.hd; a.hq = m.hq; a.hkv = m.hkv; a.rows = rows; a.q = L.q;
     a.kpre = (const char*)L.gpre + l * pre_lay;
     a.vpre = (const char*)L.gpre + l * pre_lay + pre_lay / 2;
     a.P = pl.P; a.ktail = kpool; a.vtail = vpool; a.cap = cap; a.lt = step; a.out = L.o;
     a.part = L.apart; a.part_cap = pl.apart;
-    decode_attn(a, c.s);
-    run_gemm(c, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_RESID,
-             L.h, m.d, 0);
-    ffn_block(c, G, l, L.h, L.xn, L.u, rows);
+    const double abytes = 2.0 * m.hkv * m.hd * m.es * ((double)pl.P + (double)rows * step) +
+                          (double)rows * m.hq * m.hd * (4 + m.es);
+    const double aflops = 4.0 * rows * m.hq * m.hd * ((double)pl.P + step);
+    timed(c, SR_K_DECODE_ATTN, abytes, aflops, [&] { decode_attn(a, c.s); });
+    run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_RESID, L.h,
+             m.d, 0);
+    ffn_block(c, true, G, l, L.h, L.xn, L.u, rows);
   }
-  rmsnorm(m.dtype, L.h, m.d, G.w->final_norm, m.d, m.eps, rows, L.xn, m.d, c.s);
-  run_gemm(c, m.dtype, L.xn, m.d, G.w->head, m.d, rows, m.V, m.d, EPI_STORE, L.logits, m.V, 0);
-  (void)bf;
+  run_other(c, (double)rows * m.d * (4 + m.es),
+            [&] { rmsnorm(m.dtype, L.h, m.d, G.w->final_norm, m.d, m.eps, rows, L.xn, m.d, c.s); });
+  run_gemm(c, true, m.dtype, L.xn, m.d, G.w->head, m.d, rows, m.V, m.d, EPI_STORE, L.logits, m.V, 0);
 }
 
 // Logits of the last prompt token into logits row 0 (after prompt_prefill,
@@ -391,7 +474,7 @@ static void prompt_logits(const Ctx& c, const Model& G) {
   Layout& L = *c.L;
   rmsnorm(m.dtype, L.ch + (size_t)(c.pl->P - 1) * m.d, m.d, G.w->final_norm, m.d, m.eps, 1, L.xn, m.d,
           c.s);
-  run_gemm(c, m.dtype, L.xn, m.d, G.w->head, m.d, 1, m.V, m.d, EPI_STORE, L.logits, m.V, 0);
+  run_gemm(c, false, m.dtype, L.xn, m.d, G.w->head, m.d, 1, m.V, m.d, EPI_STORE, L.logits, m.V, 0);
 }
 
 __global__ void init_state_kernel(int n, int32_t* cand, int32_t* len, int32_t* done, int32_t* cand_len,
@@ -480,7 +563,10 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   Plan pl;
   Dims gd, rd;
   Layout L = setup(gen, rm, P, p, ws, ws_bytes, &pl, &gd, &rd);
-  Ctx c{&pl, &L, s};
+  Profiler prof;
+  prof.s = s;
+  const int every = p->profile_every;
+  Ctx c{&pl, &L, s, every > 0 ? &prof : nullptr};
   Model G{gd, &gen->w}, R{rd, &rm->w};
   const int N = pl.N, Lmax = pl.Lmax;
   std::memset(out, 0, sizeof(*out));
@@ -488,6 +574,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   tall.start();
 
   // prompt prefill of both models; logits of the first response token
+  prof.active = every > 0;
   tph.start();
   rope_table(L.rope_g, P + Lmax + 1, gd.hd, gd.theta, s);
   rope_table(L.rope_r, P + Lmax + 1, rd.hd, rd.theta, s);
@@ -499,6 +586,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
                      L.st[0].len, L.st[0].done, L.cand_len, L.i_count);
   SR_CHECK_LAUNCH();
   out->sec_prefill = tph.stop();
+  prof.flush();
 
   int cur = 0;  // state/pool index of the running round
   int b = N, r = 0, step = 0;
@@ -512,6 +600,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     tph.start();
     SR_REQUIRE((int64_t)b * cap <= pl.S[cur], SR_ERR_INTERNAL, "KV pool capacity exceeded");
     for (; step < D; ++step) {
+      prof.active = every > 0 && step % every == 0;
       const State& st = L.st[cur];
       if (step > 0) decode_step(c, G, st, b, step, L.pool[cur], pl.S[cur] * gd.hkv * gd.hd, cap);
       SampleArgs sa;
@@ -519,8 +608,10 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
       sa.cand = st.cand; sa.step = step; sa.temperature = p->temperature; sa.seed = p->seed;
       sa.next_tok = st.tok; sa.done = st.done; sa.len = st.len; sa.store = L.store;
       sa.store_ld = Lmax; sa.eos_id = p->eos_id;
-      sample(sa, s);
+      timed(c, SR_K_SAMPLE, (double)b * gd.V * 4, 0.0, [&] { sample(sa, s); });
+      if (prof.active) prof.flush();
     }
+    prof.active = every > 0;
     out->sec_decode += tph.stop();
     // unfinished rows?
     h_done.resize(b);
@@ -546,7 +637,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
       ca.i_cand = L.i_cand; ca.i_len = L.i_len; ca.i_count = L.i_count; ca.i_score = L.i_score;
       ca.src_row = L.src_row; ca.cand_out = L.st[2].cand; ca.len_out = L.st[2].len;
       ca.tok_out = L.st[2].tok; ca.count = L.count;
-      cut(ca, s);
+      timed(c, SR_K_CUT, (double)b * 24, 0.0, [&] { cut(ca, s); });
       break;
     }
     // ---- phase 2: partial rewards and the cut
@@ -564,7 +655,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     ca.i_cand = L.i_cand; ca.i_len = L.i_len; ca.i_count = L.i_count; ca.i_score = L.i_score;
     ca.src_row = L.src_row; ca.cand_out = ns.cand; ca.len_out = ns.len; ca.tok_out = ns.tok;
     ca.count = L.count;
-    cut(ca, s);
+    timed(c, SR_K_CUT, (double)b * 24, 0.0, [&] { cut(ca, s); });
     // scores of the survivors, for a further cut at the same length
     int cnt = 0;
     copy_d2h(&cnt, L.count, sizeof(int32_t), s);
@@ -607,7 +698,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
       c2.i_cand = L.i_cand; c2.i_len = L.i_len; c2.i_count = L.i_count; c2.i_score = L.i_score;
       c2.src_row = L.src_row2; c2.cand_out = L.st[2].cand; c2.len_out = L.st[2].len;
       c2.tok_out = L.st[2].tok; c2.count = L.count2;
-      cut(c2, s);
+      timed(c, SR_K_CUT, (double)cnt * 24, 0.0, [&] { cut(c2, s); });
       int cnt2 = 0;
       copy_d2h(&cnt2, L.count2, sizeof(int32_t), s);
       if (tr && r < tr->max_rounds_cap) {
@@ -649,9 +740,11 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     ka.src_row = L.src_row; ka.count = L.count; ka.b = b; ka.max_rows = cnt;
     ka.n_layers = gd.nl; ka.hkv = gd.hkv; ka.hd = gd.hd; ka.elem_bytes = gd.es;
     ka.cap_src = cap; ka.cap_dst = nD; ka.len = step - 1;
-    compact(ka, s);
+    timed(c, SR_K_CUT, 4.0 * gd.nl * cnt * (double)(step - 1) * gd.hkv * gd.hd * gd.es, 0.0,
+          [&] { compact(ka, s); });
     SR_HIP(hipMemsetAsync(ns.done, 0, sizeof(int32_t) * cnt, s));
     out->sec_cut += tph.stop();
+    prof.flush();
     cur = nxt;
     b = cnt;
     D = nD;
@@ -661,7 +754,14 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   int n_i = 0;
   copy_d2h(&n_i, L.i_count, sizeof(int32_t), s);
   SR_REQUIRE(n_i >= 1 && n_i <= N, SR_ERR_INTERNAL, "set I is empty");
-  argmax_best(L.i_score, L.i_cand, L.i_count, N, L.best, s);
+  timed(c, SR_K_CUT, (double)n_i * 8, 0.0, [&] { argmax_best(L.i_score, L.i_cand, L.i_count, N, L.best, s); });
+  prof.flush();
+  for (int k = 0; k < SR_K_NCLASS; ++k) {
+    out->kernel_sec[k] = prof.sec[k];
+    out->kernel_launches[k] = prof.n[k];
+    out->kernel_bytes[k] = prof.bytes[k];
+    out->kernel_flops[k] = prof.flops[k];
+  }
   int best = -1;
   copy_d2h(&best, L.best, sizeof(int32_t), s);
   SR_REQUIRE(best >= 0 && best < n_i, SR_ERR_INTERNAL, "arg max failed");
@@ -710,7 +810,7 @@ static void teacher_forced(const sr_model* gen, const sr_model* rm, const int32_
     copy_d2h(h.data(), tokens, h.size() * sizeof(int32_t), s);
     for (int32_t t : h) SR_REQUIRE(t >= 0 && t < gd.V, SR_ERR_INVALID_ARG, "token out of range");
   }
-  Ctx c{&pl, &L, s};
+  Ctx c{&pl, &L, s, nullptr};
   Model G{gd, &gen->w};
   rope_table(L.rope_g, P + pl.Lmax + 1, gd.hd, gd.theta, s);
   copy_h2d(L.ctok, prompt, sizeof(int32_t) * P, s);
@@ -752,7 +852,7 @@ static void reward_entry(const sr_model* gen, const sr_model* rm, const int32_t*
                    SR_ERR_INVALID_ARG, "token out of range");
     }
   }
-  Ctx c{&pl, &L, s};
+  Ctx c{&pl, &L, s, nullptr};
   Model R{rd, &rm->w};
   rope_table(L.rope_r, P + pl.Lmax + 1, rd.hd, rd.theta, s);
   copy_h2d(L.ctok, prompt, sizeof(int32_t) * P, s);
