@@ -176,8 +176,10 @@ def main():
         if r:
             r["sec_timed"] = round(k["sec"], 4)
             kernels[name] = r
-    dominant = max(kern, key=lambda n: kern[n]["sec"])
-    roof = dict(kernels[dominant])
+    roof = None
+    if kernels:
+        dominant = max(kernels, key=lambda n: kernels[n]["sec_timed"])
+        roof = dict(kernels[dominant])
 
     cpu = None
     if not args.no_cpu:
