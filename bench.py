@@ -29,7 +29,7 @@ FP32_VECTOR_TFLOPS = 157.3
 # kernel class -> (bound, unit) for the implementation in this library
 BOUNDS = {
     "gen_gemm_mfma": ("mfma", "TFLOP/s"), "gen_gemm_hbm": ("hbm", "GB/s"), "decode_attn": ("hbm", "GB/s"),
-    "rm_gemm": ("mfma", "TFLOP/s"), "prefill_attn": ("alu", "TFLOP/s"), "sample": ("hbm", "GB/s"),
+    "rm_gemm": ("mfma", "TFLOP/s"), "prefill_attn": ("mfma", "TFLOP/s"), "sample": ("hbm", "GB/s"),
     "cut": ("hbm", "GB/s"), "other": ("hbm", "GB/s"),
 }
 

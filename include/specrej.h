@@ -237,6 +237,22 @@ sr_status sr_compact(const void *src, int64_t src_block_elems, void *dst,
                      int32_t cap_src, int32_t cap_dst, int32_t len, int32_t *src_row,
                      int32_t *new_count, void *stream);
 
+/* One projection of the decoder (the dense contraction of sections a3, a5,
+ * a6 and a7 of the hot path): with X [M][K] and W [N][K] (dtype elements,
+ * row-major, DEVICE),
+ *   mode 0: out (float [M][N])  = X W^T
+ *   mode 1: out (float [M][N]) += X W^T                      (residual add)
+ *   mode 2: out (dtype [M][N])  = silu(X W1^T) * (X W3^T)     (SwiGLU; W holds
+ *           [2][N][K]: W1 rows then W3 rows)
+ *   mode 3: out (dtype [M][N])  = X W^T
+ * fp32 accumulation.  partial: DEVICE float scratch of partial_elems >=
+ * sr_projection_scratch(dtype, M, N, K, mode) elements (may be NULL when that
+ * is 0).  K must be a multiple of 64.  Asynchronous. */
+sr_status sr_projection(int32_t dtype, const void *x, const void *w, int32_t M, int32_t N,
+                        int32_t K, int32_t mode, void *out, float *partial, size_t partial_elems,
+                        void *stream);
+size_t sr_projection_scratch(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t mode);
+
 /* Teacher-forced generator logits through the decode path: all `rows`
  * continue `prompt` (HOST int32 [prompt_len]) with their own tokens
  * (DEVICE int32 [rows][len]); logits_out (DEVICE float [rows][len][vocab])

@@ -98,7 +98,10 @@ def lib():
                                                _i32, _vp, _vp, ctypes.c_size_t, _vp]
         L.sr_reward_scores.argtypes = [P(sr_model), P(sr_model), _vp, _i32, P(sr_params), _vp, _vp, _i32,
                                        _i32, _vp, _vp, ctypes.c_size_t, _vp]
-        for f in ("sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
+        L.sr_projection.argtypes = [_i32, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, ctypes.c_size_t, _vp]
+        L.sr_projection_scratch.argtypes = [_i32, _i32, _i32, _i32, _i32]
+        L.sr_projection_scratch.restype = ctypes.c_size_t
+        for f in ("sr_projection", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
                   "sr_logits_teacher_forced", "sr_reward_scores"):
             getattr(L, f).restype = _i32
         _lib = L
@@ -237,6 +240,19 @@ def compact(src, src_block, dst, dst_block, keep_flag, n_layers, n_kv_heads, hea
     _check(lib().sr_compact(_ptr(src), src_block, _ptr(dst), dst_block, _ptr(keep_flag), keep_flag.shape[0],
                             n_layers, n_kv_heads, head_dim, elem_bytes, cap_src, cap_dst, length, _ptr(src_row),
                             _ptr(new_count), _stream(stream)))
+
+
+def projection(x, w, mode: int, out, stream=None):
+    """sr_projection: x [M][K], w [N][K] (mode 2: [2][N][K]), see the header."""
+    import torch
+    dtype = SR_BF16 if x.dtype in (torch.int16, torch.bfloat16) else SR_F32
+    M, K = x.shape
+    N = w.shape[-2]
+    need = int(lib().sr_projection_scratch(dtype, M, N, K, mode))
+    part = torch.empty(max(need, 1), dtype=torch.float32, device=x.device)
+    _check(lib().sr_projection(dtype, _ptr(x), _ptr(w), M, N, K, mode, _ptr(out), _ptr(part), need,
+                               _stream(stream)))
+    return part
 
 
 def logits_teacher_forced(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, tokens, ws: Workspace,

@@ -340,6 +340,143 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
   }
 }
 
+
+// --------------------------------------------------------- prefill (MFMA)
+// bf16 flash attention with v_mfma_f32_16x16x32_bf16.  Work-group = one row,
+// one KV head, 16 queries; wave w computes query head (kvh * G + w) for those
+// queries, so the G waves share every K/V tile staged in LDS (32 keys).
+//   S^T = K Q^T   (keys x queries): lane l holds keys 4(l/16)+i (+16 for the
+//                 second key tile) of query l%16, so the online-softmax state
+//                 of a query lives in one lane group (max/sum over l/16).
+//   O^T += V^T P^T (dims x queries): the key order of this contraction is
+//                 permuted so that the B operand is exactly the lane's own
+//                 S^T values (keys 4g..4g+3 of tile 0, then of tile 1); the A
+//                 operand reads V^T, staged transposed in LDS, at those keys.
+constexpr int PF_KT = 32;            // keys per tile
+constexpr int PF_KROW = 128 + 8;     // K tile row (bf16), padded
+constexpr int PF_VROW = 32 + 4;      // V^T tile row (bf16), padded
+
+template <int G>
+__global__ void __launch_bounds__(64 * G)
+prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
+                         const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
+                         const bf16_t* __restrict__ vown, int lr, int hq, int hkv, bf16_t* __restrict__ out,
+                         float qscale) {
+  constexpr int HD = 128, NT = 64 * G;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * PF_VROW];
+  const int qb = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int qh = h * G + wave;
+  const int t = qb * 16 + fr;              // this lane's query (as B column / C column)
+  const bool qvalid = t < lr;
+  // Q^T fragments: lane holds Q[t][32 s + 8 fg .. +8] for k-step s (scaled, bf16)
+  bf16x8 qf[4];
+  {
+    const float* qr = q + (((int64_t)row * lr + (qvalid ? t : 0)) * hq + qh) * HD;
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = qvalid ? qr[32 * st + 8 * fg + e] * qscale : 0.f;
+        qf[st][e] = (__bf16)v;
+      }
+  }
+  f32x4 o[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  const int tlast = min(lr, (qb + 1) * 16) - 1;
+  const int nkeys = P + tlast + 1;
+  const bf16_t* kp = kpre + (int64_t)h * P * HD;
+  const bf16_t* vp = vpre + (int64_t)h * P * HD;
+  const bf16_t* ko = kown + ((int64_t)row * hkv + h) * lr * HD;
+  const bf16_t* vo = vown + ((int64_t)row * hkv + h) * lr * HD;
+  for (int kb = 0; kb < nkeys; kb += PF_KT) {
+    // stage K [key][dim] and V^T [dim][key]: 32 keys x 16 chunks of 8 dims
+    for (int c = threadIdx.x; c < PF_KT * 16; c += NT) {
+      const int j = c >> 4, cc = c & 15;
+      const int key = kb + j;
+      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      if (key < nkeys) {
+        const bf16_t* kr = key < P ? kp + (int64_t)key * HD : ko + (int64_t)(key - P) * HD;
+        const bf16_t* vr = key < P ? vp + (int64_t)key * HD : vo + (int64_t)(key - P) * HD;
+        kv = *reinterpret_cast<const uint4*>(kr + cc * 8);
+        vv = *reinterpret_cast<const uint4*>(vr + cc * 8);
+      }
+      *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kv;
+      const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        Vt[(cc * 8 + 2 * e) * PF_VROW + j] = (bf16_t)(w4[e] & 0xFFFFu);
+        Vt[(cc * 8 + 2 * e + 1) * PF_VROW + j] = (bf16_t)(w4[e] >> 16);
+      }
+    }
+    __syncthreads();
+    // S^T for key tiles 0 (keys kb..kb+15) and 1 (kb+16..kb+31)
+    f32x4 st[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(kt * 16 + fr) * PF_KROW + 32 * s + 8 * fg]);
+        st[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[kt], 0, 0, 0);
+      }
+    }
+    // causal mask and tile maximum for query t (this lane's column)
+    float mt = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kb + kt * 16 + 4 * fg + i;
+        const bool ok = qvalid && key < nkeys && key <= P + t;
+        st[kt][i] = ok ? st[kt][i] : -INFINITY;
+        mt = fmaxf(mt, st[kt][i]);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m, mt);
+    const float corr = (mn == -INFINITY) ? 1.f : exp2_or_zero(m - mn);
+    float ls = 0.f;
+    bf16x8 pf;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = (mn == -INFINITY) ? 0.f : exp2_or_zero(st[kt][i] - mn);
+        ls += p;
+        pf[kt * 4 + i] = (__bf16)p;
+      }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    l = l * corr + ls;
+    m = mn;
+    // O^T += V^T P^T over the 32 keys in the permuted order
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      o[dt] *= corr;
+      const bf16_t* vr = &Vt[(dt * 16 + fr) * PF_VROW];
+      const uint2 a0 = *reinterpret_cast<const uint2*>(vr + 4 * fg);
+      const uint2 a1 = *reinterpret_cast<const uint2*>(vr + 16 + 4 * fg);
+      const uint4 a = make_uint4(a0.x, a0.y, a1.x, a1.y);
+      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&a);
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[dt], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  if (qvalid) {
+    const float inv = 1.0f / l;
+    bf16_t* orow = out + (((int64_t)row * lr + t) * hq + qh) * HD;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
+  }
+}
+
 template <typename T, int HD, int G>
 static void launch_prefill(const PrefillAttnArgs& a, hipStream_t s) {
   constexpr int QB = 64 / G;
@@ -372,8 +509,27 @@ static void prefill_by_hd(const PrefillAttnArgs& a, hipStream_t s) {
   }
 }
 
+template <int G>
+static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
+  const float qscale = kLog2e / sqrtf(128.f);
+  dim3 grid((a.lr + 15) / 16, a.hkv, a.rows);
+  hipLaunchKernelGGL(prefill_attn_mfma_kernel<G>, grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
+                     (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.hq, a.hkv,
+                     (bf16_t*)a.out, qscale);
+  SR_CHECK_LAUNCH();
+}
+
 void prefill_attn(const PrefillAttnArgs& a, hipStream_t s) {
   if (a.rows <= 0 || a.lr <= 0) return;
+  if (a.dtype == SR_BF16 && a.hd == 128) {
+    switch (a.hq / a.hkv) {
+      case 1: launch_prefill_mfma<1>(a, s); return;
+      case 2: launch_prefill_mfma<2>(a, s); return;
+      case 4: launch_prefill_mfma<4>(a, s); return;
+      case 8: launch_prefill_mfma<8>(a, s); return;
+      default: break;
+    }
+  }
   if (a.dtype == SR_BF16) prefill_by_hd<bf16_t>(a, s);
   else prefill_by_hd<float>(a, s);
 }

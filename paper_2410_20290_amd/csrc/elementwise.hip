@@ -132,6 +132,158 @@ void rope_scatter(int dtype, const float* qkv, int rows, int lr, int hq, int hkv
   SR_CHECK_LAUNCH();
 }
 
+// One block per row: h = E[tok]; xn = RMSNorm(h) * g.
+template <typename T>
+__global__ void __launch_bounds__(256)
+embed_norm_kernel(const T* __restrict__ E, int d, const int32_t* __restrict__ tok, const T* __restrict__ g,
+                  float eps, float* __restrict__ h, T* __restrict__ xn) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const T* src = E + (int64_t)tok[r] * d;
+  float* hr = h + (int64_t)r * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = to_f32<T>(src[i]);
+    hr[i] = v;
+    ss += v * v;
+  }
+  ss = block_sum256(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  T* o = xn + (int64_t)r * d;
+  for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f32<T>(hr[i] * inv * to_f32<T>(g[i]));
+}
+
+void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, const void* g, float eps,
+                float* h, void* xn, hipStream_t s) {
+  if (rows <= 0) return;
+  if (dtype == SR_BF16)
+    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, (const bf16_t*)E, d, tok,
+                       (const bf16_t*)g, eps, h, (bf16_t*)xn);
+  else
+    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)E, d, tok,
+                       (const float*)g, eps, h, (float*)xn);
+  SR_CHECK_LAUNCH();
+}
+
+// One block per row: h += sum of split partials (in split order); xn = RMSNorm(h) * g.
+// Threads own float4 column chunks; the chunks of one thread (up to 4 per
+// pass) are independent, so their loads are in flight together.
+template <typename T>
+__global__ void __launch_bounds__(256)
+add_norm_kernel(const float* __restrict__ part, int splits, int rows, int d, float* __restrict__ h,
+                const T* __restrict__ g, float eps, T* __restrict__ xn) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const int d4 = d / 4;
+  float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
+  const float4* pr = reinterpret_cast<const float4*>(part + (int64_t)r * d);
+  const int64_t sstride4 = (int64_t)rows * d4;
+  float ss = 0.f;
+  for (int base = 0; base < d4; base += 4 * 256) {
+    float4 v[4];
+    bool ok[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = base + u * 256 + threadIdx.x;
+      ok[u] = j < d4;
+      v[u] = ok[u] ? hr[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    for (int sp = 0; sp < splits; ++sp) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = base + u * 256 + threadIdx.x;
+        if (ok[u]) {
+          const float4 p = pr[sp * sstride4 + j];
+          v[u].x += p.x; v[u].y += p.y; v[u].z += p.z; v[u].w += p.w;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = base + u * 256 + threadIdx.x;
+      if (ok[u]) {
+        hr[j] = v[u];
+        ss += v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
+      }
+    }
+  }
+  ss = block_sum256(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  const float* hs = h + (int64_t)r * d;
+  T* o = xn + (int64_t)r * d;
+  for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f32<T>(hs[i] * inv * to_f32<T>(g[i]));
+}
+
+void add_norm(int dtype, const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
+              void* xn, hipStream_t s) {
+  if (rows <= 0) return;
+  SR_REQUIRE(d % 4 == 0, 3, "d_model must be a multiple of 4");
+  if (dtype == SR_BF16)
+    hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, part, splits, rows, d, h,
+                       (const bf16_t*)g, eps, (bf16_t*)xn);
+  else
+    hipLaunchKernelGGL(add_norm_kernel<float>, dim3(rows), dim3(256), 0, s, part, splits, rows, d, h,
+                       (const float*)g, eps, (float*)xn);
+  SR_CHECK_LAUNCH();
+}
+
+// Grid (rows, hq + 2 hkv), one wave per (row, head): sum the split partials
+// of the head, rotate q and k heads, scatter.
+template <typename T>
+__global__ void __launch_bounds__(64)
+qkv_finalize_kernel(const float* __restrict__ part, int splits, int rows, int hq, int hkv, int hd,
+                    const float2* __restrict__ tab, int pos, float* __restrict__ qout, T* __restrict__ kdst,
+                    T* __restrict__ vdst, int cap, int t0) {
+  const int r = blockIdx.x, head = blockIdx.y;
+  const int qkv_dim = (hq + 2 * hkv) * hd;
+  const int64_t sstride = (int64_t)rows * qkv_dim;
+  const float* src = part + (int64_t)r * qkv_dim + head * hd;
+  const int half = hd / 2;
+  if (head < hq + hkv) {
+    const float2* cs = tab + (int64_t)pos * half;
+    for (int i = threadIdx.x; i < half; i += 64) {
+      float x1 = 0.f, x2 = 0.f;
+      for (int sp = 0; sp < splits; ++sp) {
+        x1 += src[sp * sstride + i];
+        x2 += src[sp * sstride + half + i];
+      }
+      const float2 c = cs[i];
+      const float y1 = x1 * c.x - x2 * c.y;
+      const float y2 = x2 * c.x + x1 * c.y;
+      if (head < hq) {
+        float* qo = qout + ((int64_t)r * hq + head) * hd;
+        qo[i] = y1;
+        qo[half + i] = y2;
+      } else {
+        T* ko = kdst + (((int64_t)r * hkv + (head - hq)) * cap + t0) * hd;
+        ko[i] = from_f32<T>(y1);
+        ko[half + i] = from_f32<T>(y2);
+      }
+    }
+  } else {
+    T* vo = vdst + (((int64_t)r * hkv + (head - hq - hkv)) * cap + t0) * hd;
+    for (int i = threadIdx.x; i < hd; i += 64) {
+      float x = 0.f;
+      for (int sp = 0; sp < splits; ++sp) x += src[sp * sstride + i];
+      vo[i] = from_f32<T>(x);
+    }
+  }
+}
+
+void qkv_finalize(int dtype, const float* part, int splits, int rows, int hq, int hkv, int hd,
+                  const float2* tab, int pos, float* qout, void* kdst, void* vdst, int cap, int t0,
+                  hipStream_t s) {
+  if (rows <= 0) return;
+  dim3 grid(rows, hq + 2 * hkv);
+  if (dtype == SR_BF16)
+    hipLaunchKernelGGL(qkv_finalize_kernel<bf16_t>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
+                       pos, qout, (bf16_t*)kdst, (bf16_t*)vdst, cap, t0);
+  else
+    hipLaunchKernelGGL(qkv_finalize_kernel<float>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
+                       pos, qout, (float*)kdst, (float*)vdst, cap, t0);
+  SR_CHECK_LAUNCH();
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256)
 score_head_kernel(const float* __restrict__ h, int d, int lr, const int32_t* __restrict__ len,

@@ -6,6 +6,8 @@
 // buffering.  fp32: a plain LDS-tiled FMA kernel (used by the fp32 model).
 // Split-K writes fp32 partials [split][M][Nout] that a second kernel sums in
 // split order, so results do not depend on scheduling.
+#include <cstdlib>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -38,6 +40,44 @@ __device__ __forceinline__ void epi_one(const EpiArgs& e, int m, int n, float v)
   }
 }
 
+// ------------------------------------------------------------ tile order
+// Work-groups are dealt round-robin to the 8 XCDs, each with its own L2.  A
+// 1-D grid of 8 * C groups is remapped so that XCD x runs the consecutive
+// logical tiles [x C, (x + 1) C); logical tiles are ordered split-major, then
+// in groups of up to 8 row tiles with the row tile fastest, so tiles that
+// share a weight panel (same column tile and split) run on one XCD at about
+// the same time, and tiles that share an activation panel stay close.
+struct TileIdx {
+  int m, n, split;
+  bool valid;
+};
+
+__device__ __forceinline__ TileIdx tile_of(int nm, int nn, int splits) {
+  const int total = nm * nn * splits;
+  const int per_xcd = (total + 7) / 8;
+  const int g = blockIdx.x;
+  const int pid = (g % 8) * per_xcd + g / 8;
+  TileIdx t;
+  t.valid = pid < total;
+  const int per_split = nm * nn;
+  t.split = pid / per_split;
+  const int q = pid % per_split;
+  const int gm = min(nm, 8);
+  const int in_group = gm * nn;
+  const int grp = q / in_group;
+  const int first_m = grp * gm;
+  const int size_m = min(nm - first_m, gm);
+  const int r = q % in_group;
+  t.m = first_m + r % size_m;
+  t.n = r / size_m;
+  return t;
+}
+
+static inline dim3 tile_grid(int nm, int nn, int splits) {
+  const int total = nm * nn * splits;
+  return dim3(8 * ((total + 7) / 8));
+}
+
 // ------------------------------------------------------------ bf16 MFMA GEMM
 // Block tile BM x BN (x2 when PAIRED: gate rows n and up rows pair_off + n),
 // K step BK, wave tile WM x WN.  PAIRED epilogue: silu(gate) * up.
@@ -58,11 +98,13 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
   __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDS_ROW];
   __shared__ __attribute__((aligned(16))) bf16_t Bs[2][NB * BN * LDS_ROW];
 
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, K / k_per_split);
+  if (!tile.valid) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / (BN / WN)) * WM, wn0 = (wave % (BN / WN)) * WN;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int k_begin = blockIdx.z * k_per_split;
+  const int m0 = tile.m * BM, n0 = tile.n * BN;
+  const int k_begin = tile.split * k_per_split;
   const int k_end = min(K, k_begin + k_per_split);
   const int nk = (k_end - k_begin) / BK;
 
@@ -163,7 +205,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
         if (m >= M || n >= N) continue;
         if (partial) {
           const int nout = NB * N;
-          float* p = partial + ((int64_t)blockIdx.z * M + m) * nout;
+          float* p = partial + ((int64_t)tile.split * M + m) * nout;
           p[n] = acc[0][i][j][e];
           if (PAIRED) p[N + n] = acc[NB - 1][i][j][e];
         } else if (PAIRED) {
@@ -172,6 +214,145 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
           epi_one(epi, m, n, acc[0][i][j][e]);
         }
       }
+}
+
+
+// ------------------------------------------------- bf16 MFMA GEMM, large M
+// 256 x 256 block tile (PAIRED: 128 output columns, gate and up rows
+// interleaved in groups of 32 so one wave holds both for its columns),
+// K step 64, 4 waves each owning a 128 x 128 tile of 4 x 4
+// v_mfma_f32_32x32x16_bf16 accumulators (256 fp32 per lane).  The next K
+// tile is fetched into registers while the current one is multiplied from
+// LDS; ~2k MFMA cycles per wave per iteration cover the fetch latency.
+template <bool PAIRED>
+__global__ void __launch_bounds__(256)
+gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                float* __restrict__ partial) {
+  constexpr int BM = 256, BNL = 256, BK = 64, PAD = 8, LDS_ROW = BK + PAD;
+  constexpr int BN_OUT = PAIRED ? 128 : 256;   // output columns per block
+  constexpr int CH_ROW = BK / 8;               // 8 chunks of 16 B per row
+  constexpr int IT = BM * CH_ROW / 256;        // 8 chunks per thread (A and B alike)
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDS_ROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BNL * LDS_ROW];
+
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN_OUT - 1) / BN_OUT, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave >> 1) * 128, wn0 = (wave & 1) * 128;
+  const int m0 = tile.m * BM, n0 = tile.n * BN_OUT;
+  const int k_begin = tile.split * k_per_split;
+  const int k_end = min(K, k_begin + k_per_split);
+  const int nk = (k_end - k_begin) / BK;
+
+  // B row of LDS row r
+  auto brow = [&](int r, int64_t* off, int* n) {
+    if (PAIRED) {
+      const int grp = r >> 5, blk = grp & 1;
+      *n = n0 + (grp >> 1) * 32 + (r & 31);
+      *off = blk * pair_off;
+    } else {
+      *n = n0 + r;
+      *off = 0;
+    }
+  };
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  uint4 ra[IT], rb[IT];
+  auto load_global = [&](int kt) {
+    const int kb = k_begin + kt * BK;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int c = tid + it * 256;
+      const int r = c / CH_ROW, cc = c % CH_ROW;
+      const int m = m0 + r;
+      ra[it] = m < M ? *reinterpret_cast<const uint4*>(A + (int64_t)m * lda + kb + cc * 8)
+                     : make_uint4(0, 0, 0, 0);
+      int64_t off;
+      int n;
+      brow(r, &off, &n);
+      rb[it] = n < N ? *reinterpret_cast<const uint4*>(B + off + (int64_t)n * ldb + kb + cc * 8)
+                     : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_lds = [&](int buf) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int c = tid + it * 256;
+      const int r = c / CH_ROW, cc = c % CH_ROW;
+      *reinterpret_cast<uint4*>(&As[buf][r * LDS_ROW + cc * 8]) = ra[it];
+      *reinterpret_cast<uint4*>(&Bs[buf][r * LDS_ROW + cc * 8]) = rb[it];
+    }
+  };
+
+  if (nk > 0) {
+    load_global(0);
+    store_lds(0);
+  }
+  __syncthreads();
+  const int fr = lane & 31, fg = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_global(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 16) {
+      bf16x8 af[4], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(&As[buf][(wm0 + i * 32 + fr) * LDS_ROW + ks + fg * 8]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(wn0 + j * 32 + fr) * LDS_ROW + ks + fg * 8]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) store_lds(buf ^ 1);
+    __syncthreads();
+  }
+
+  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
+      if (m >= M) continue;
+      if (PAIRED) {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int n = n0 + (wn0 >> 1) + jj * 32 + fr;
+          if (n >= N) continue;
+          const float g = acc[i][2 * jj][e], u = acc[i][2 * jj + 1][e];
+          if (partial) {
+            float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
+            p[n] = g;
+            p[N + n] = u;
+          } else {
+            store_out(epi, m, n, silu(g) * u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = n0 + wn0 + j * 32 + fr;
+          if (n >= N) continue;
+          if (partial)
+            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
+          else
+            epi_one(epi, m, n, acc[i][j][e]);
+        }
+      }
+    }
 }
 
 // ------------------------------------------------------------ fp32 GEMM
@@ -252,7 +433,7 @@ template <int BM, int BN, int BK, int WM, int WN, bool PAIRED>
 static void launch_bf16(const GemmArgs& g, int splits, int kps, const EpiArgs& e, float* part,
                         hipStream_t s) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
-  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, splits);
+  dim3 grid = tile_grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, splits);
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WM, WN, PAIRED>), grid, dim3(NT), 0, s,
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N,
                      g.K, kps, e, part);
@@ -265,10 +446,30 @@ size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired) {
   return (size_t)p.splits * M * (paired ? 2 * (size_t)N : (size_t)N);
 }
 
+// Partials needed by an EPI_PARTIAL call (written even without a K split).
+size_t gemm_partial_elems_always(int dtype, int M, int N, int K) {
+  GemmPlan p = gemm_plan(dtype, M, N, K, false);
+  return (size_t)p.splits * M * (size_t)N;
+}
+
+// Rows from which the 256 x 256 tile is used.
+static int big_tile_min_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_BIG_TILE_MIN_M");
+    return e ? atoi(e) : 1024;
+  }();
+  return v;
+}
+
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
+  p.big = false;
   if (dtype != SR_BF16) return p;
+  if (M >= big_tile_min_rows()) {
+    p.big = true;
+    return p;
+  }
   int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
   int bn = paired ? 64 : 128;
   int64_t tiles = (int64_t)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
@@ -281,10 +482,11 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   return p;
 }
 
-void gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
+int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   SR_REQUIRE(g.K % 64 == 0, 3, "GEMM K must be a multiple of 64");
+  SR_REQUIRE(!(g.epi == EPI_PARTIAL && g.paired), 5, "partial epilogue is for unpaired projections");
   EpiArgs e{g.epi, g.out, g.ldo, g.out_bf16};
-  if (g.M == 0 || g.N == 0) return;
+  if (g.M == 0 || g.N == 0) return 1;
   if (g.dtype == SR_F32) {
     const int ncols = (g.paired ? 2 : 1) * g.N;
     SR_REQUIRE((size_t)g.M * ncols <= partial_cap, 5, "GEMM partial buffer too small");
@@ -292,24 +494,35 @@ void gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) 
     hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, (const float*)g.A, g.lda,
                        (const float*)g.B, g.ldb, g.pair_off, (int)g.paired, g.M, g.N, g.K, partial);
     SR_CHECK_LAUNCH();
+    if (g.epi == EPI_PARTIAL) return 1;
     int64_t total = (int64_t)g.M * g.N;
     int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, partial, 1, g.M, g.N,
                        (int)g.paired, e);
     SR_CHECK_LAUNCH();
-    return;
+    return 1;
   }
   GemmPlan plan = gemm_plan(g.dtype, g.M, g.N, g.K, g.paired);
   const int splits = plan.splits;
   const int kps = g.K / splits;
   SR_REQUIRE(kps * splits == g.K && kps % 64 == 0, 5, "split-K must divide K into multiples of 64");
   float* part = nullptr;
-  if (splits > 1) {
+  if (splits > 1 || g.epi == EPI_PARTIAL) {
     SR_REQUIRE((size_t)splits * g.M * (g.paired ? 2 : 1) * (size_t)g.N <= partial_cap, 5,
                "GEMM partial buffer too small");
     part = partial;
   }
-  if (g.paired) {
+  if (plan.big) {
+    const int bn_out = g.paired ? 128 : 256;
+    dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
+    if (g.paired)
+      hipLaunchKernelGGL(gemm_big_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+    else
+      hipLaunchKernelGGL(gemm_big_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+    SR_CHECK_LAUNCH();
+  } else if (g.paired) {
     if (g.M <= 32) launch_bf16<32, 64, 64, 32, 16, true>(g, splits, kps, e, part, s);
     else if (g.M <= 64) launch_bf16<64, 64, 64, 32, 32, true>(g, splits, kps, e, part, s);
     else launch_bf16<128, 64, 64, 64, 32, true>(g, splits, kps, e, part, s);
@@ -318,13 +531,14 @@ void gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) 
     else if (g.M <= 64) launch_bf16<64, 128, 64, 32, 64, false>(g, splits, kps, e, part, s);
     else launch_bf16<128, 128, 64, 64, 64, false>(g, splits, kps, e, part, s);
   }
-  if (splits > 1) {
+  if (splits > 1 && g.epi != EPI_PARTIAL) {
     int64_t total = (int64_t)g.M * g.N;
     int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, g.M, g.N,
                        (int)g.paired, e);
     SR_CHECK_LAUNCH();
   }
+  return splits;
 }
 
 }  // namespace sr

@@ -146,6 +146,12 @@ static Plan make_plan(const Dims& g, const Dims& rm, int P, const sr_params* p) 
       size_t ncol = std::max({(size_t)m->qkv, (size_t)m->d, (size_t)2 * m->ff, (size_t)m->V});
       gp = std::max(gp, (size_t)Mmax * ncol);
     } else {
+      if (m == &g)
+        for (int M = 1; M <= pl.N; ++M) {
+          gp = std::max(gp, gemm_partial_elems_always(m->dtype, M, m->qkv, m->d));
+          gp = std::max(gp, gemm_partial_elems_always(m->dtype, M, m->d, m->hq * m->hd));
+          gp = std::max(gp, gemm_partial_elems_always(m->dtype, M, m->d, m->ff));
+        }
       for (int M = 1; M <= Mmax; ++M) {
         gp = std::max(gp, gemm_partial_elems(m->dtype, M, m->qkv, m->d, false));
         gp = std::max(gp, gemm_partial_elems(m->dtype, M, m->d, m->hq * m->hd, false));
@@ -329,20 +335,22 @@ static void timed(const Ctx& c, int cls, double bytes, double flops, F&& launch)
 
 // Projection launch.  decode: a generator decode projection (classed by
 // whether its rows make it MFMA- or weight-bound), else reward/prefill.
-static void run_gemm(const Ctx& c, bool decode, int dtype, const void* A, int lda, const void* B, int ldb,
-                     int M, int N, int K, int epi, void* out, int ldo, int out_bf16, bool paired = false,
-                     int64_t pair_off = 0) {
+static int run_gemm(const Ctx& c, bool decode, int dtype, const void* A, int lda, const void* B, int ldb,
+                    int M, int N, int K, int epi, void* out, int ldo, int out_bf16, bool paired = false,
+                    int64_t pair_off = 0) {
   GemmArgs g;
   g.dtype = dtype; g.A = A; g.lda = lda; g.B = B; g.ldb = ldb; g.pair_off = pair_off;
   g.paired = paired; g.M = M; g.N = N; g.K = K; g.epi = epi; g.out = out; g.ldo = ldo;
   g.out_bf16 = out_bf16;
   const double es = dtype == SR_BF16 ? 2.0 : 4.0;
   const double nw = paired ? 2.0 * N : (double)N;
-  double ob = epi == EPI_RESID ? 8.0 : (paired || out_bf16 ? es : 4.0);
+  double ob = epi == EPI_RESID ? 8.0 : (epi == EPI_PARTIAL ? 4.0 : (paired || out_bf16 ? es : 4.0));
   const double bytes = es * ((double)M * K + nw * K) + ob * (double)M * N;
   const double flops = 2.0 * M * nw * K;
   const int cls = decode ? (M >= 312 ? SR_K_GEN_GEMM_MFMA : SR_K_GEN_GEMM_HBM) : SR_K_RM_GEMM;
-  timed(c, cls, bytes, flops, [&] { gemm(g, c.L->gpart, c.pl->gpart, c.s); });
+  int splits = 1;
+  timed(c, cls, bytes, flops, [&] { splits = gemm(g, c.L->gpart, c.pl->gpart, c.s); });
+  return splits;
 }
 
 static void run_other(const Ctx& c, double bytes, std::function<void()> f) {
@@ -436,17 +444,18 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
   const Dims& m = G.m;
   Layout& L = *c.L;
   const Plan& pl = *c.pl;
-  run_other(c, (double)rows * m.d * (4 + m.es), [&] { embed(m.dtype, G.w->embed, m.d, st.tok, rows, L.h, c.s); });
+  const int bf = m.dtype == SR_BF16;
+  run_other(c, (double)rows * m.d * (4 + m.es), [&] {
+    embed_norm(m.dtype, G.w->embed, m.d, st.tok, rows, G.attn_norm(0), m.eps, L.h, L.xn, c.s);
+  });
   const size_t pre_lay = (size_t)2 * m.hkv * pl.P * m.hd * m.es;
   for (int l = 0; l < m.nl; ++l) {
     char* kpool = (char*)pool + (size_t)(2 * l) * pool_block * m.es;
     char* vpool = (char*)pool + (size_t)(2 * l + 1) * pool_block * m.es;
-    run_other(c, (double)rows * m.d * (4 + m.es),
-              [&] { rmsnorm(m.dtype, L.h, m.d, G.attn_norm(l), m.d, m.eps, rows, L.xn, m.d, c.s); });
-    run_gemm(c, true, m.dtype, L.xn, m.d, G.wqkv(l), m.d, rows, m.qkv, m.d, EPI_STORE, L.qkv, m.qkv, 0);
-    run_other(c, (double)rows * (m.qkv * 4.0 + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
-      rope_scatter(m.dtype, L.qkv, rows, 1, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool, vpool, cap,
-                   step - 1, c.s);
+    int sp = run_gemm(c, true, m.dtype, L.xn, m.d, G.wqkv(l), m.d, rows, m.qkv, m.d, EPI_PARTIAL, nullptr, 0, 0);
+    run_other(c, (double)rows * (m.qkv * 4.0 * sp + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
+      qkv_finalize(m.dtype, L.gpart, sp, rows, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool, vpool,
+                   cap, step - 1, c.s);
     });
     DecodeAttnArgs a;
     a.dtype = m.dtype; a.hd = m.hd; a.hq = m.hq; a.hkv = m.hkv; a.rows = rows; a.q = L.q;
@@ -458,12 +467,19 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
                           (double)rows * m.hq * m.hd * (4 + m.es);
     const double aflops = 4.0 * rows * m.hq * m.hd * ((double)pl.P + step);
     timed(c, SR_K_DECODE_ATTN, abytes, aflops, [&] { decode_attn(a, c.s); });
-    run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_RESID, L.h,
-             m.d, 0);
-    ffn_block(c, true, G, l, L.h, L.xn, L.u, rows);
+    sp = run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_PARTIAL,
+                  nullptr, 0, 0);
+    run_other(c, (double)rows * m.d * (4.0 * sp + 8 + m.es), [&] {
+      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, G.ffn_norm(l), m.eps, L.xn, c.s);
+    });
+    run_gemm(c, true, m.dtype, L.xn, m.d, G.w13(l), m.d, rows, m.ff, m.d, EPI_STORE, L.u, m.ff, bf, true,
+             (int64_t)m.ff * m.d);
+    sp = run_gemm(c, true, m.dtype, L.u, m.ff, G.w2(l), m.ff, rows, m.d, m.ff, EPI_PARTIAL, nullptr, 0, 0);
+    const void* gnext = l + 1 < m.nl ? G.attn_norm(l + 1) : G.w->final_norm;
+    run_other(c, (double)rows * m.d * (4.0 * sp + 8 + m.es), [&] {
+      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, gnext, m.eps, L.xn, c.s);
+    });
   }
-  run_other(c, (double)rows * m.d * (4 + m.es),
-            [&] { rmsnorm(m.dtype, L.h, m.d, G.w->final_norm, m.d, m.eps, rows, L.xn, m.d, c.s); });
   run_gemm(c, true, m.dtype, L.xn, m.d, G.w->head, m.d, rows, m.V, m.d, EPI_STORE, L.logits, m.V, 0);
 }
 
@@ -987,6 +1003,32 @@ sr_status sr_compact(const void* src, int64_t src_block_elems, void* dst, int64_
     a.scratch_src_row = src_row;
     a.new_count = new_count;
     compact(a, (hipStream_t)stream);
+  });
+}
+
+size_t sr_projection_scratch(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t mode) {
+  if (M < 0 || N < 0 || K < 0 || mode < 0 || mode > 3) return 0;
+  if (dtype == SR_F32) return (size_t)M * (mode == 2 ? 2 * (size_t)N : (size_t)N);
+  return gemm_partial_elems(dtype, M, N, K, mode == 2);
+}
+
+sr_status sr_projection(int32_t dtype, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
+                        int32_t mode, void* out, float* partial, size_t partial_elems, void* stream) {
+  return guard([&] {
+    SR_REQUIRE(dtype == SR_F32 || dtype == SR_BF16, SR_ERR_INVALID_ARG, "unknown dtype");
+    SR_REQUIRE(M >= 0 && N >= 1 && K >= 1, SR_ERR_INVALID_ARG, "bad M/N/K");
+    SR_REQUIRE(mode >= 0 && mode <= 3, SR_ERR_INVALID_ARG, "mode must be 0..3");
+    SR_REQUIRE(K % 64 == 0, SR_ERR_UNSUPPORTED, "K must be a multiple of 64");
+    SR_REQUIRE(M == 0 || (x && w && out), SR_ERR_INVALID_ARG, "NULL buffer");
+    const size_t need = sr_projection_scratch(dtype, M, N, K, mode);
+    SR_REQUIRE(partial_elems >= need && (need == 0 || partial), SR_ERR_WORKSPACE_TOO_SMALL,
+               "partial scratch too small: need " + std::to_string(need) + " floats");
+    GemmArgs g;
+    g.dtype = dtype; g.A = x; g.lda = K; g.B = w; g.ldb = K; g.paired = mode == 2;
+    g.pair_off = (int64_t)N * K; g.M = M; g.N = N; g.K = K;
+    g.epi = mode == 1 ? EPI_RESID : EPI_STORE; g.out = out; g.ldo = N;
+    g.out_bf16 = (mode == 2 || mode == 3) && dtype == SR_BF16;
+    gemm(g, partial, partial_elems, (hipStream_t)stream);
   });
 }
 

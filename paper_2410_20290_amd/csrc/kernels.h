@@ -9,7 +9,7 @@
 namespace sr {
 
 // ---- GEMM -------------------------------------------------------------------
-enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1 };
+enum GemmEpi { EPI_STORE = 0, EPI_RESID = 1, EPI_PARTIAL = 2 };
 
 struct GemmArgs {
   int dtype;             // SR_F32 / SR_BF16: element type of A and B
@@ -20,17 +20,21 @@ struct GemmArgs {
   int64_t pair_off;      // elements between the gate and up blocks (paired only)
   bool paired;           // out = silu(A B_gate^T) * (A B_up^T)
   int M, N, K;
-  int epi;               // EPI_STORE (out = C) or EPI_RESID (fp32 out += C); paired: store
+  int epi;               // EPI_STORE (out = C), EPI_RESID (fp32 out += C) or EPI_PARTIAL
+                         // (fp32 split partials [splits][M][N] left in `partial` for a
+                         // fused consumer; gemm() returns the split count); paired: store
   void* out;
   int ldo;
   int out_bf16;          // EPI_STORE / paired: 1 = bf16 out, 0 = fp32 out
 };
 struct GemmPlan {
   int splits;
+  bool big;  // 256 x 256 tile kernel
 };
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired);
 size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired);
-void gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s);
+int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s);
+size_t gemm_partial_elems_always(int dtype, int M, int N, int K);
 
 // ---- elementwise / small ------------------------------------------------------
 // h[r][:] = float(E[tok[r]][:]), r < rows.
@@ -53,6 +57,18 @@ void score_head(int dtype, const float* h, int d, int lr, const int32_t* len, in
 void gather_tokens(const int32_t* store, int ld, const int32_t* cand, const int32_t* len, int rows,
                    int lr, int32_t* tokens, hipStream_t s);
 void philox_fill(uint64_t seed, const uint32_t* ctr, int n, uint32_t* out, hipStream_t s);
+// h[r] = E[tok[r]] (fp32); xn[r] = RMSNorm(h[r]) * g (model dtype).
+void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, const void* g, float eps,
+                float* h, void* xn, hipStream_t s);
+// h[r] += sum_s part[s][r]; xn[r] = RMSNorm(h[r]) * g (model dtype); d columns.
+void add_norm(int dtype, const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
+              void* xn, hipStream_t s);
+// qkv[r] = sum_s part[s][r] (rows of (hq + 2 hkv) hd); RoPE at position pos
+// on q and k; q -> qout[r][hq][hd] (fp32); k, v -> kdst/vdst[r][hkv][cap][hd]
+// at token t0.
+void qkv_finalize(int dtype, const float* part, int splits, int rows, int hq, int hkv, int hd,
+                  const float2* tab, int pos, float* qout, void* kdst, void* vdst, int cap, int t0,
+                  hipStream_t s);
 
 // ---- attention ----------------------------------------------------------------
 // Decode: one query per row at the newest position.  Keys: the shared prefix

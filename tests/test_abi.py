@@ -25,12 +25,12 @@ def L():
 
 def declared_symbols():
     text = open(os.path.join(ROOT, "include", "specrej.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:sr_status|int32_t|const char \*)\s*\*?(sr_\w+)\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:sr_status|int32_t|size_t|const char \*)\s*\*?(sr_\w+)\(", text, re.M)))
 
 
 def test_header_symbols_exported(L):
     names = declared_symbols()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(L, n), n
 

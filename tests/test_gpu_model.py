@@ -47,3 +47,39 @@ def test_reward_scores(name):
     _, orm = oracle_models(name)
     ref = np.array([orm.score(list(prompt) + list(toks[r, :lens[r]])) for r in range(rows)])
     assert np.abs(got - ref).max() <= tol(c) * np.abs(ref).max(), (got, ref)
+
+
+def _hd128_shape(g):
+    import synth
+    hkv = 2
+    return synth.ModelShape(2, 128 * hkv * g if g > 1 else 256, hkv * g, hkv, 128, 512, 1000, "bf16", 500000.0)
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8])
+def test_reward_and_logits_head_dim_128(g):
+    """head_dim 128 paths (MFMA prefill attention, 128-wide decode) for every
+    GQA group size, on small random bf16 models."""
+    import synth
+    from oracle.transformer import Transformer
+    torch, sr = need_gpu()
+    shape = _hd128_shape(g)
+    say(f"hd128 g={g} shape={shape}")
+    gw, rw = synth.model_weights(shape, 0, False), synth.model_weights(shape, 1, True)
+    gen, rm = sr.DeviceModel.upload(shape, gw, False), sr.DeviceModel.upload(shape, rw, True)
+    prompt = synth.tokens(37, shape.vocab, 5)
+    rng = np.random.default_rng(g)
+    rows, max_len = 5, 45
+    toks = rng.integers(0, shape.vocab, size=(rows, max_len)).astype(np.int32)
+    lens = np.array([45, 1, 17, 33, 44], dtype=np.int32)
+    p = sr.make_params(8, 0.5, 45, 48)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    got = sr.reward_scores(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(),
+                           ws).cpu().numpy()
+    orm = Transformer(shape, rw, True)
+    ref = np.array([orm.score(list(prompt) + list(toks[r, :lens[r]])) for r in range(rows)])
+    assert np.abs(got - ref).max() <= 2e-2 * np.abs(ref).max(), (got, ref)
+    lg = sr.logits_teacher_forced(gen, rm, prompt, p, torch.from_numpy(toks[:3, :20].copy()).cuda(), ws).cpu().numpy()
+    og = Transformer(shape, gw, False)
+    for r in range(3):
+        refl = og.logits(list(prompt) + list(toks[r, :20]))[len(prompt) - 1: len(prompt) - 1 + 20]
+        assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max()
