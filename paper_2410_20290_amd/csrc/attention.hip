@@ -25,17 +25,18 @@ __global__ void __launch_bounds__(256)
 decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, const T* __restrict__ vpre,
                    int P, const T* __restrict__ ktail, const T* __restrict__ vtail, int cap, int lt,
                    int hq, int hkv, int kps, int splits, float* __restrict__ part,
-                   T* __restrict__ out, float qscale) {
+                   T* __restrict__ out, float qscale, int key0, int split0) {
   constexpr int EPL = Vec16<T>::N;   // elements per 16-byte load
   constexpr int LPK = HD / EPL;      // lanes per key row
   constexpr int KPW = 64 / LPK;      // keys per wave step
   constexpr int U = 4;               // keys per lane per iteration
   constexpr int NW = 4;              // waves
+  // keys [key0, P + lt) in splits of kps; partial slot split0 + split
   const int split = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sub = lane % LPK, ks = lane / LPK;
   const int total = P + lt;
-  const int k0 = split * kps, k1 = min(total, k0 + kps);
+  const int k0 = key0 + split * kps, k1 = min(total, k0 + kps);
 
   float qv[G][EPL];
 #pragma unroll
@@ -57,35 +58,39 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
   const T* kp = kpre + (int64_t)h * P * HD;
   const T* vp = vpre + (int64_t)h * P * HD;
 
-  for (int base = k0; base < k1; base += NW * KPW * U) {
-    float kf[U][EPL], vf[U][EPL];
+  // Raw 16-byte loads of the next U keys are issued before the current U
+  // keys are consumed (two register sets, unrolled by two).
+  constexpr int STEP = NW * KPW * U;
+  uint4 rk0[U], rv0[U], rk1[U], rv1[U];
+  auto fetch = [&](int base, uint4 (&rk)[U], uint4 (&rv)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = min(base + (u * NW + wave) * KPW + ks, k1 - 1);
+      const T* kr = (j < P) ? kp + (int64_t)j * HD : kt + (int64_t)(j - P) * HD;
+      const T* vr = (j < P) ? vp + (int64_t)j * HD : vt + (int64_t)(j - P) * HD;
+      rk[u] = *reinterpret_cast<const uint4*>(kr + sub * EPL);
+      rv[u] = *reinterpret_cast<const uint4*>(vr + sub * EPL);
+    }
+  };
+  auto consume = [&](int base, const uint4 (&rk)[U], const uint4 (&rv)[U]) {
+    float s[U][G];
     bool valid[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = base + (u * NW + wave) * KPW + ks;
       valid[u] = j < k1;
-      if (valid[u]) {
-        const T* kr = (j < P) ? kp + (int64_t)j * HD : kt + (int64_t)(j - P) * HD;
-        const T* vr = (j < P) ? vp + (int64_t)j * HD : vt + (int64_t)(j - P) * HD;
-        Vec16<T>::load(kr + sub * EPL, kf[u]);
-        Vec16<T>::load(vr + sub * EPL, vf[u]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) kf[u][e] = vf[u][e] = 0.f;
-      }
-    }
-    float s[U][G];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
+      float kf[EPL];
+      Vec16<T>::load(reinterpret_cast<const T*>(&rk[u]), kf);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float d = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) d = fmaf(qv[g][e], kf[u][e], d);
+        for (int e = 0; e < EPL; ++e) d = fmaf(qv[g][e], kf[e], d);
 #pragma unroll
         for (int o = LPK / 2; o > 0; o >>= 1) d += __shfl_xor(d, o, 64);
         s[u][g] = valid[u] ? d : -INFINITY;
       }
+    }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       float mt = s[0][g];
@@ -97,14 +102,28 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
       l[g] *= corr;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) acc[g][e] *= corr;
+      m[g] = mn;
+    }
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float p = exp2_or_zero(s[u][g] - mn);
+    for (int u = 0; u < U; ++u) {
+      float vf[EPL];
+      Vec16<T>::load(reinterpret_cast<const T*>(&rv[u]), vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float p = (m[g] == -INFINITY) ? 0.f : exp2_or_zero(s[u][g] - m[g]);
         l[g] += p;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[u][e], acc[g][e]);
+        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
       }
-      m[g] = mn;
+    }
+  };
+  if (k0 < k1) {
+    fetch(k0, rk0, rv0);
+    for (int base = k0; base < k1; base += 2 * STEP) {
+      fetch(base + STEP, rk1, rv1);
+      consume(base, rk0, rv0);
+      fetch(base + 2 * STEP, rk0, rv0);
+      if (base + STEP < k1) consume(base + STEP, rk1, rv1);
     }
   }
 
@@ -160,7 +179,7 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
     if (splits == 1) {
       out[((int64_t)row * hq + qh) * HD + dd] = from_f32<T>(A / L);
     } else {
-      float* p = part + (((int64_t)row * hq + qh) * splits + split) * (HD + 2);
+      float* p = part + (((int64_t)row * hq + qh) * splits + split0 + split) * (HD + 2);
       p[dd] = A;
       if (dd == 0) {
         p[HD] = M;
@@ -188,33 +207,66 @@ __global__ void decode_merge_kernel(const float* __restrict__ part, int splits, 
   }
 }
 
-// Keys per split: aim for enough work-groups to fill the chip, at least 256
+// Keys per split: aim for enough work-groups to fill the chip, at least 128
 // keys per split.
 static int decode_kps(int rows, int hkv, int keys) {
   int64_t groups = (int64_t)rows * hkv;
   int splits = 1;
-  while (groups * splits < 1024 && keys / (splits * 2) >= 256) splits *= 2;
+  while (groups * splits < 2048 && keys / (splits * 2) >= 128) splits *= 2;
   return (keys + splits - 1) / splits;
 }
 
+template <int G, bool PREFIX_ONLY>
+__global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
+                                         const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
+                                         const bf16_t* __restrict__ vown, int lr, int hq, int hkv,
+                                         bf16_t* __restrict__ out, float qscale, float* __restrict__ part,
+                                         int part_splits);
+
+// Whether the shared prefix is attended by the batched MFMA kernel.
+static bool prefix_by_mfma(int dtype, int hd, int P) { return dtype == SR_BF16 && hd == 128 && P > 0; }
+
+// Partial slots needed for `keys` = prefix + maximal tail (upper bound for
+// both the combined and the split-prefix forms).
 int decode_attn_splits(int rows, int hkv, int keys) {
   int kps = decode_kps(rows, hkv, keys);
-  return (keys + kps - 1) / kps;
+  return (keys + kps - 1) / kps + (keys + 63) / 64;
 }
 
 template <typename T, int HD, int G>
 static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
+  const float qscale = kLog2e / sqrtf((float)HD);
+  if (prefix_by_mfma(a.dtype, HD, a.P)) {
+    // prefix partials (slots 0..psplits-1, 64 keys each, 16 rows per
+    // work-group), then the tail partials
+    const int psplits = (a.P + 63) / 64;
+    const int tkps = decode_kps(a.rows, a.hkv, a.lt);
+    const int tsplits = (a.lt + tkps - 1) / tkps;
+    const int splits = tsplits + psplits;
+    SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
+    hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits), dim3(64 * G),
+                       0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows,
+                       a.hq, a.hkv, nullptr, qscale, a.part, splits);
+    SR_CHECK_LAUNCH();
+    hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
+                       (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail, (const T*)a.vtail, a.cap, a.lt,
+                       a.hq, a.hkv, tkps, splits, a.part, (T*)a.out, qscale, a.P, psplits);
+    SR_CHECK_LAUNCH();
+    hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, splits, a.hq,
+                       (T*)a.out);
+    SR_CHECK_LAUNCH();
+    return;
+  }
   const int keys = a.P + a.lt;
   const int kps = decode_kps(a.rows, a.hkv, keys);
   const int splits = (keys + kps - 1) / kps;
   if (splits > 1)
     SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5,
                "attention partial buffer too small");
-  const float qscale = kLog2e / sqrtf((float)HD);
   hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(splits, a.hkv, a.rows), dim3(256), 0, s,
                      a.q, (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail,
                      (const T*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (T*)a.out,
-                     qscale);
+                     qscale, 0, 0);
   SR_CHECK_LAUNCH();
   if (splits > 1) {
     hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part,
@@ -356,16 +408,21 @@ constexpr int PF_KT = 32;            // keys per tile
 constexpr int PF_KROW = 128 + 8;     // K tile row (bf16), padded
 constexpr int PF_VROW = 32 + 4;      // V^T tile row (bf16), padded
 
-template <int G>
+// PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
+// The 16 "queries" of a work-group are 16 decode rows (lr = rows, one
+// sequence), every prefix key is visible, and the unnormalised output with
+// its running max and sum is written as split 0 of the decode partials.
+template <int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
                          const bf16_t* __restrict__ vown, int lr, int hq, int hkv, bf16_t* __restrict__ out,
-                         float qscale) {
+                         float qscale, float* __restrict__ part, int part_splits) {
   constexpr int HD = 128, NT = 64 * G;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * PF_VROW];
-  const int qb = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
+  // PREFIX_ONLY: blockIdx.z is the prefix split (keys [64 z, 64 z + 64)).
+  const int qb = blockIdx.x, h = blockIdx.y, row = PREFIX_ONLY ? 0 : blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const int qh = h * G + wave;
@@ -388,12 +445,13 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
   const int tlast = min(lr, (qb + 1) * 16) - 1;
-  const int nkeys = P + tlast + 1;
+  const int kbeg = PREFIX_ONLY ? blockIdx.z * 64 : 0;
+  const int nkeys = PREFIX_ONLY ? min(P, kbeg + 64) : P + tlast + 1;
   const bf16_t* kp = kpre + (int64_t)h * P * HD;
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
-  const bf16_t* ko = kown + ((int64_t)row * hkv + h) * lr * HD;
-  const bf16_t* vo = vown + ((int64_t)row * hkv + h) * lr * HD;
-  for (int kb = 0; kb < nkeys; kb += PF_KT) {
+  const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * lr * HD;
+  const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * lr * HD;
+  for (int kb = kbeg; kb < nkeys; kb += PF_KT) {
     // stage K [key][dim] and V^T [dim][key]: 32 keys x 16 chunks of 8 dims
     for (int c = threadIdx.x; c < PF_KT * 16; c += NT) {
       const int j = c >> 4, cc = c & 15;
@@ -432,7 +490,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kb + kt * 16 + 4 * fg + i;
-        const bool ok = qvalid && key < nkeys && key <= P + t;
+        const bool ok = qvalid && key < nkeys && (PREFIX_ONLY || key <= P + t);
         st[kt][i] = ok ? st[kt][i] : -INFINITY;
         mt = fmaxf(mt, st[kt][i]);
       }
@@ -468,12 +526,24 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     __syncthreads();
   }
   if (qvalid) {
-    const float inv = 1.0f / l;
-    bf16_t* orow = out + (((int64_t)row * lr + t) * hq + qh) * HD;
+    if (PREFIX_ONLY) {
+      float* pr = part + (((int64_t)t * hq + qh) * part_splits + blockIdx.z) * (HD + 2);
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
+      for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
+        for (int i = 0; i < 4; ++i) pr[dt * 16 + 4 * fg + i] = o[dt][i];
+      if (fg == 0) {
+        pr[HD] = m;
+        pr[HD + 1] = l;
+      }
+    } else {
+      const float inv = 1.0f / l;
+      bf16_t* orow = out + (((int64_t)row * lr + t) * hq + qh) * HD;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
+    }
   }
 }
 
@@ -513,9 +583,9 @@ template <int G>
 static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf(128.f);
   dim3 grid((a.lr + 15) / 16, a.hkv, a.rows);
-  hipLaunchKernelGGL(prefill_attn_mfma_kernel<G>, grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
+  hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
                      (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.hq, a.hkv,
-                     (bf16_t*)a.out, qscale);
+                     (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();
 }
 

@@ -214,10 +214,64 @@ add_norm_kernel(const float* __restrict__ part, int splits, int rows, int d, flo
   for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f32<T>(hs[i] * inv * to_f32<T>(g[i]));
 }
 
+// Row-parallel form for few rows: grid (rows, ceil(d / 1024)).  The first
+// kernel adds the split partials into h and leaves each block's sum of
+// squares; the second sums those in block order and normalises.
+__global__ void __launch_bounds__(256)
+add_rows_kernel(const float* __restrict__ part, int splits, int rows, int d, float* __restrict__ h,
+                float* __restrict__ ssp) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, blk = blockIdx.y, nblk = gridDim.y;
+  const int d4 = d / 4;
+  const int j = blk * 256 + threadIdx.x;
+  float ss = 0.f;
+  if (j < d4) {
+    float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
+    const float4* pr = reinterpret_cast<const float4*>(part + (int64_t)r * d);
+    const int64_t sstride4 = (int64_t)rows * d4;
+    float4 v = hr[j];
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4 p = pr[sp * sstride4 + j];
+      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    hr[j] = v;
+    ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum256(ss, red);
+  if (threadIdx.x == 0) ssp[(int64_t)r * nblk + blk] = ss;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+norm_rows_kernel(const float* __restrict__ h, int d, const float* __restrict__ ssp, const T* __restrict__ g,
+                 float eps, T* __restrict__ xn) {
+  const int r = blockIdx.x, blk = blockIdx.y, nblk = gridDim.y;
+  float ss = 0.f;
+  for (int b = 0; b < nblk; ++b) ss += ssp[(int64_t)r * nblk + b];
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  const int c0 = blk * 1024, c1 = min(d, c0 + 1024);
+  const float* hr = h + (int64_t)r * d;
+  T* o = xn + (int64_t)r * d;
+  for (int i = c0 + threadIdx.x; i < c1; i += 256) o[i] = from_f32<T>(hr[i] * inv * to_f32<T>(g[i]));
+}
+
 void add_norm(int dtype, const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
-              void* xn, hipStream_t s) {
+              void* xn, float* ssp, hipStream_t s) {
   if (rows <= 0) return;
   SR_REQUIRE(d % 4 == 0, 3, "d_model must be a multiple of 4");
+  if (ssp && rows < 256) {
+    dim3 grid(rows, (d + 1023) / 1024);
+    hipLaunchKernelGGL(add_rows_kernel, grid, dim3(256), 0, s, part, splits, rows, d, h, ssp);
+    SR_CHECK_LAUNCH();
+    if (dtype == SR_BF16)
+      hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, grid, dim3(256), 0, s, h, d, ssp, (const bf16_t*)g, eps,
+                         (bf16_t*)xn);
+    else
+      hipLaunchKernelGGL(norm_rows_kernel<float>, grid, dim3(256), 0, s, h, d, ssp, (const float*)g, eps,
+                         (float*)xn);
+    SR_CHECK_LAUNCH();
+    return;
+  }
   if (dtype == SR_BF16)
     hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, part, splits, rows, d, h,
                        (const bf16_t*)g, eps, (bf16_t*)xn);

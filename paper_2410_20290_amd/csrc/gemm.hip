@@ -117,31 +117,26 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
       for (int j = 0; j < TN; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   uint4 ra[A_IT], rb[B_IT];
+  // unconditional loads (rows clamped, out-of-range rows zeroed by a select)
   auto load_global = [&](int kt) {
     const int kb = k_begin + kt * BK;
 #pragma unroll
     for (int it = 0; it < A_IT; ++it) {
-      int c = tid + it * NT;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c < A_CH) {
-        int r = c / CH_ROW, cc = c % CH_ROW;
-        int m = m0 + r;
-        if (m < M) v = *reinterpret_cast<const uint4*>(A + (int64_t)m * lda + kb + cc * 8);
-      }
-      ra[it] = v;
+      const int c = min(tid + it * NT, A_CH - 1);
+      const int r = c / CH_ROW, cc = c % CH_ROW;
+      const int m = m0 + r;
+      const uint4 v = *reinterpret_cast<const uint4*>(A + (int64_t)min(m, M - 1) * lda + kb + cc * 8);
+      ra[it] = m < M ? v : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int it = 0; it < B_IT; ++it) {
-      int c = tid + it * NT;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (c < B_CH) {
-        int r = c / CH_ROW, cc = c % CH_ROW;
-        int blk = r / BN, rr = r % BN;
-        int n = n0 + rr;
-        if (n < N)
-          v = *reinterpret_cast<const uint4*>(B + blk * pair_off + (int64_t)n * ldb + kb + cc * 8);
-      }
-      rb[it] = v;
+      const int c = min(tid + it * NT, B_CH - 1);
+      const int r = c / CH_ROW, cc = c % CH_ROW;
+      const int blk = r / BN, rr = r % BN;
+      const int n = n0 + rr;
+      const uint4 v =
+          *reinterpret_cast<const uint4*>(B + blk * pair_off + (int64_t)min(n, N - 1) * ldb + kb + cc * 8);
+      rb[it] = n < N ? v : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_lds = [&](int buf) {
@@ -273,13 +268,13 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
       const int c = tid + it * 256;
       const int r = c / CH_ROW, cc = c % CH_ROW;
       const int m = m0 + r;
-      ra[it] = m < M ? *reinterpret_cast<const uint4*>(A + (int64_t)m * lda + kb + cc * 8)
-                     : make_uint4(0, 0, 0, 0);
+      const uint4 va = *reinterpret_cast<const uint4*>(A + (int64_t)min(m, M - 1) * lda + kb + cc * 8);
+      ra[it] = m < M ? va : make_uint4(0, 0, 0, 0);
       int64_t off;
       int n;
       brow(r, &off, &n);
-      rb[it] = n < N ? *reinterpret_cast<const uint4*>(B + off + (int64_t)n * ldb + kb + cc * 8)
-                     : make_uint4(0, 0, 0, 0);
+      const uint4 vb = *reinterpret_cast<const uint4*>(B + off + (int64_t)min(n, N - 1) * ldb + kb + cc * 8);
+      rb[it] = n < N ? vb : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_lds = [&](int buf) {
@@ -350,6 +345,145 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
             partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
           else
             epi_one(epi, m, n, acc[i][j][e]);
+        }
+      }
+    }
+}
+
+
+// -------------------------------------------- bf16 MFMA GEMM, few rows
+// For M <= 128 (decode after the cuts) the weights dominate: every weight
+// element is used by only M rows.  Work-group = 4 waves over 128 output
+// columns (PAIRED: 64 columns, each wave holding gate and up of its 16), all
+// M rows padded to 16 * TM.  The activation chunk (rows x 128 of K) is staged
+// in LDS once and shared by the 4 waves; each wave streams its weight rows
+// straight into registers, two chunks ahead of the MFMAs.
+template <int TM, bool PAIRED>
+__global__ void __launch_bounds__(256)
+gemm_skinny_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                   int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                   float* __restrict__ partial) {
+  constexpr int KC = 128, AROW = KC + 8, MP = TM * 16;
+  constexpr int COLS = PAIRED ? 64 : 128;
+  constexpr int A_CH = MP * (KC / 8);                 // 16-byte chunks of an A chunk
+  constexpr int A_IT = (A_CH + 255) / 256;
+  __shared__ __attribute__((aligned(16))) bf16_t As[2][MP * AROW];
+  const TileIdx tile = tile_of(1, (N + COLS - 1) / COLS, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int fr = lane & 15, fg = lane >> 4;
+  const int n0 = tile.n * COLS;
+  const int kb = tile.split * k_per_split;
+  const int nch = k_per_split / KC;
+  // this lane's two weight rows (fragment f = 0, 1)
+  const bf16_t* brow[2];
+  int ncol[2];
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    const int n = PAIRED ? n0 + wave * 16 + fr : n0 + wave * 32 + f * 16 + fr;
+    ncol[f] = n;
+    const int nc = min(n, N - 1);
+    brow[f] = B + ((PAIRED && f == 1) ? pair_off : 0) + (int64_t)nc * ldb + kb + fg * 8;
+  }
+  f32x4 acc[TM][2];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int f = 0; f < 2; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Weight fragments: a ring of three chunks with static slots (the chunk
+  // loop is unrolled by three), so chunk c + 2 is requested at the top of
+  // iteration c, two chunks of MFMAs ahead of its use.
+  bf16x8 bq0[4][2], bq1[4][2], bq2[4][2];
+  // Loads are unconditional (chunk index and rows clamped, out-of-range rows
+  // zeroed by a select) so that the wait counts stay exact across the loop.
+  auto load_b = [&](int c, bf16x8 (&dst)[4][2]) {
+    const int cc = min(c, nch - 1);
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+        dst[st][f] = *reinterpret_cast<const bf16x8*>(brow[f] + cc * KC + st * 32);
+  };
+  uint4 ra[A_IT];
+  auto load_a = [&](int c) {
+    const int cc = min(c, nch - 1);
+#pragma unroll
+    for (int it = 0; it < A_IT; ++it) {
+      const int ch = min(tid + it * 256, A_CH - 1);
+      const int r = ch / (KC / 8), k8 = ch % (KC / 8);
+      const uint4 v = *reinterpret_cast<const uint4*>(A + (int64_t)min(r, M - 1) * lda + kb + cc * KC + k8 * 8);
+      ra[it] = r < M ? v : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int it = 0; it < A_IT; ++it) {
+      const int ch = tid + it * 256;
+      if (ch < A_CH) {
+        const int r = ch / (KC / 8), cc = ch % (KC / 8);
+        *reinterpret_cast<uint4*>(&As[buf][r * AROW + cc * 8]) = ra[it];
+      }
+    }
+  };
+  auto step = [&](int c, bf16x8 (&cur)[4][2], bf16x8 (&ahead)[4][2]) {
+    const int buf = c & 1;
+    load_b(c + 2, ahead);
+    load_a(c + 1);
+    if (c < nch) {
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const bf16x8 af =
+              *reinterpret_cast<const bf16x8*>(&As[buf][(i * 16 + fr) * AROW + st * 32 + fg * 8]);
+#pragma unroll
+          for (int f = 0; f < 2; ++f)
+            acc[i][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, cur[st][f], acc[i][f], 0, 0, 0);
+        }
+      }
+    }
+    store_a(buf ^ 1);
+    __syncthreads();
+  };
+
+  load_b(0, bq0);
+  load_b(1, bq1);
+  load_a(0);
+  store_a(0);
+  __syncthreads();
+  for (int c = 0; c < nch; c += 3) {
+    step(c, bq0, bq2);
+    step(c + 1, bq1, bq0);
+    step(c + 2, bq2, bq1);
+  }
+
+  // lane holds rows 16 i + 4 (lane/16) + e of column fragment f
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = i * 16 + fg * 4 + e;
+      if (m >= M) continue;
+      if (PAIRED) {
+        const int n = ncol[0];
+        if (n >= N) continue;
+        if (partial) {
+          float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
+          p[n] = acc[i][0][e];
+          p[N + n] = acc[i][1][e];
+        } else {
+          store_out(epi, m, n, silu(acc[i][0][e]) * acc[i][1][e]);
+        }
+      } else {
+#pragma unroll
+        for (int f = 0; f < 2; ++f) {
+          const int n = ncol[f];
+          if (n >= N) continue;
+          if (partial)
+            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][f][e];
+          else
+            epi_one(epi, m, n, acc[i][f][e]);
         }
       }
     }
@@ -461,13 +595,46 @@ static int big_tile_min_rows() {
   return v;
 }
 
+static int skinny_max_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_SKINNY_MAX_M");
+    return e ? atoi(e) : 0;
+  }();
+  return v;
+}
+
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
   p.big = false;
+  p.skinny = false;
   if (dtype != SR_BF16) return p;
   if (M >= big_tile_min_rows()) {
     p.big = true;
+    return p;
+  }
+  if (M <= skinny_max_rows() && K % 128 == 0) {
+    // Enough work-groups to fill every CU to its occupancy (fewer rows use
+    // fewer registers and allow more resident work-groups); splits divide K
+    // into multiples of 128.
+    p.skinny = true;
+    const int cols = paired ? 64 : 128;
+    const int64_t tiles = (N + cols - 1) / cols;
+    const int chunks = K / 128;
+    const int tm = (M + 15) / 16;
+    static const int per_cu_env = [] {
+      const char* e = getenv("SPECREJ_SKINNY_WG_PER_CU");
+      return e ? atoi(e) : 0;
+    }();
+    const int per_cu = per_cu_env > 0 ? per_cu_env : (tm <= 2 ? 4 : (tm <= 4 ? 3 : 2));
+    const int64_t target = 256LL * per_cu;
+    int splits = 1;
+    for (int sp = 1; sp <= chunks && sp <= 64; ++sp) {
+      if (chunks % sp) continue;
+      splits = sp;
+      if (tiles * sp >= target) break;
+    }
+    p.splits = splits;
     return p;
   }
   int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
@@ -512,7 +679,35 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
                "GEMM partial buffer too small");
     part = partial;
   }
-  if (plan.big) {
+  if (plan.skinny) {
+    const int cols = g.paired ? 64 : 128;
+    dim3 grid = tile_grid(1, (g.N + cols - 1) / cols, splits);
+    const int tm = (g.M + 15) / 16;
+#define SR_SKINNY(TM)                                                                                \
+  hipLaunchKernelGGL((gemm_skinny_kernel<TM, PAIRED_>), grid, dim3(256), 0, s, (const bf16_t*)g.A, \
+                     g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part)
+#define SR_SKINNY_ALL()                                   \
+  switch (tm) {                                           \
+    case 1: SR_SKINNY(1); break;                          \
+    case 2: SR_SKINNY(2); break;                          \
+    case 3: SR_SKINNY(3); break;                          \
+    case 4: SR_SKINNY(4); break;                          \
+    case 5: SR_SKINNY(5); break;                          \
+    case 6: SR_SKINNY(6); break;                          \
+    case 7: SR_SKINNY(7); break;                          \
+    default: SR_SKINNY(8); break;                         \
+  }
+    if (g.paired) {
+      constexpr bool PAIRED_ = true;
+      SR_SKINNY_ALL();
+    } else {
+      constexpr bool PAIRED_ = false;
+      SR_SKINNY_ALL();
+    }
+#undef SR_SKINNY_ALL
+#undef SR_SKINNY
+    SR_CHECK_LAUNCH();
+  } else if (plan.big) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
     if (g.paired)
