@@ -52,6 +52,19 @@ def roofline_of(name, k, dtype):
             "avg_launch_us": round(k["sec"] / max(1, k["launches"]) * 1e6, 2), "launches_timed": k["launches"]}
 
 
+def load_traffic(kernel_class):
+    """HBM traffic per launch of a kernel class from the committed PMC
+    summary (profiles/traffic_*.json, written from rocprofv3 --pmc runs of
+    FETCH_SIZE and WRITE_SIZE scaled by a copy of known size), if it was
+    taken for this class; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    return {"bytes_per_launch": d["traffic_bytes_per_launch"], "source": os.path.relpath(path, ROOT)}
+
+
 def cpu_baseline(cfg, gw, rows, steps, prompt_len):
     """The oracle's batched decode on the same generator, bounded sample."""
     import numpy as np
@@ -91,7 +104,7 @@ def main():
     ap.add_argument("--no-bon", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
-    ap.add_argument("--cpu-steps", type=int, default=6)
+    ap.add_argument("--cpu-steps", type=int, default=48)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the hot path is one GPU's batch of "
@@ -170,16 +183,26 @@ def main():
         del wsb
         torch.cuda.empty_cache()
 
+    # Decode-step launches are timed in 1 of every `profile_every` steps,
+    # reward/prefill/cut launches always: scale to estimate each class's
+    # share of the run when picking the dominant one.
+    decode_classes = {"gen_gemm_mfma", "gen_gemm_hbm", "decode_attn", "sample"}
     kernels = {}
     for name, k in kern.items():
         r = roofline_of(name, k, m.dtype)
         if r:
             r["sec_timed"] = round(k["sec"], 4)
+            r["sec_est_per_step"] = round(k["sec"] * (args.profile_every if name in decode_classes else 1)
+                                          / args.steps, 4)
             kernels[name] = r
     roof = None
     if kernels:
-        dominant = max(kernels, key=lambda n: kernels[n]["sec_timed"])
+        dominant = max(kernels, key=lambda n: kernels[n]["sec_est_per_step"])
         roof = dict(kernels[dominant])
+        tr = load_traffic(dominant)
+        if tr:
+            roof["traffic"] = tr["bytes_per_launch"]
+            roof["traffic_source"] = tr["source"]
 
     cpu = None
     if not args.no_cpu:

@@ -1,0 +1,99 @@
+"""Measurement launches for profiling (run under rocprofv3 from any cwd).
+
+    python3 <repo>/paper_2410_20290_amd/probes.py traffic
+        A 1 GiB device copy (to scale the FETCH_SIZE / WRITE_SIZE counters),
+        then the decode projections of the 8B-shaped generator at 103 and at
+        21 rows, three launches each; prints the algorithmic bytes of each.
+    python3 <repo>/paper_2410_20290_amd/probes.py gemm [rows,rows,...]
+        Graph-replay timing of the projections at the given row counts.
+"""
+import json
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+SHAPES = [("qkv", 6144, 4096, 0), ("o", 4096, 4096, 1), ("w13", 14336, 4096, 2), ("w2", 4096, 14336, 1),
+          ("head", 128256, 4096, 0)]
+
+
+def _operands(torch, M, N, K, mode):
+    import paper_2410_20290_amd as sr
+    nw = 2 * N if mode == 2 else N
+    x = torch.randn(M, K, device="cuda").to(torch.bfloat16).view(torch.int16)
+    w = (torch.randn(nw, K, device="cuda") * 0.02).to(torch.bfloat16).view(torch.int16)
+    out = torch.zeros(M, N, device="cuda", dtype=torch.float32 if mode in (0, 1) else torch.int16)
+    need = int(sr.lib().sr_projection_scratch(1, M, N, K, mode))
+    part = torch.empty(max(need, 1), dtype=torch.float32, device="cuda")
+    return x, w, out, part, need, nw
+
+
+def _launch(torch, x, w, out, part, need, M, N, K, mode):
+    import paper_2410_20290_amd as sr
+    st = sr.lib().sr_projection(1, x.data_ptr(), w.data_ptr(), M, N, K, mode, out.data_ptr(), part.data_ptr(),
+                                need, torch.cuda.current_stream().cuda_stream)
+    if st != 0:
+        raise RuntimeError(sr.last_error())
+
+
+def traffic():
+    import torch
+    n = 256 << 20
+    a = torch.ones(n, device="cuda")
+    b = torch.empty(n, device="cuda")
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print("copy_bytes", 4 * n, flush=True)
+    for M in (103, 21):
+        for name, N, K, mode in SHAPES:
+            x, w, out, part, need, nw = _operands(torch, M, N, K, mode)
+            torch.cuda.synchronize()
+            for _ in range(3):
+                _launch(torch, x, w, out, part, need, M, N, K, mode)
+            torch.cuda.synchronize()
+            alg = 2 * (nw * K + M * K) + M * N * (8 if mode == 1 else (2 if mode == 2 else 4))
+            print("shape", M, name, N, K, mode, alg, flush=True)
+
+
+def gemm(rows):
+    import torch
+
+    def gtime(f, reps=10):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            f()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                f()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (2 * reps) * 1e-3
+
+    for M in rows:
+        for name, N, K, mode in SHAPES:
+            if name == "head" and M > 512:
+                continue
+            x, w, out, part, need, nw = _operands(torch, M, N, K, mode)
+            t = gtime(lambda: _launch(torch, x, w, out, part, need, M, N, K, mode))
+            fl = 2.0 * M * nw * K
+            by = 2.0 * (nw * K + M * K) + M * N * 4
+            print(json.dumps({"M": M, "op": name, "us": round(t * 1e6, 1), "TFLOPs": round(fl / t / 1e12, 1),
+                              "GBs": round(by / t / 1e9)}), flush=True)
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "traffic":
+        traffic()
+    else:
+        gemm([int(v) for v in (sys.argv[2] if len(sys.argv) > 2 else "21,103,512,4096,32768").split(",")])
