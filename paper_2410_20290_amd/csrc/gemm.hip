@@ -351,6 +351,219 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 }
 
 
+// ------------------------------------- bf16 MFMA GEMM, LDS-DMA pipeline
+// 256 x 256 block tile (PAIRED: gate and up rows interleaved in groups of 32,
+// 128 output columns), K step 64, two LDS stages of 64 KB.  Operand tiles go
+// from memory straight into LDS with global_load_lds_dwordx4 (no staging
+// registers); each instruction moves 8 rows of 128 bytes, so every request
+// to L2 is a whole 128-byte line.  A K step is four quarter steps of 16
+// MFMAs per wave (4 waves, each a 128 x 128 tile of 4 x 4
+// v_mfma_f32_32x32x16_bf16 accumulators); the fragment reads of the next
+// quarter and the DMAs of the step after next run between the MFMAs, and the
+// one barrier per step sits before the last quarter.  LDS rows hold eight
+// 16-byte chunks; chunk c of tile row r sits in slot c ^ (r & 7) ^ ((r >> 3) & 3)
+// (a function of r mod 32, so fragment blocks of 32 rows share it), which puts the fragment reads of any 8 or 16 consecutive rows on distinct
+// banks.
+#define SR_VM_BARRIER(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+template <bool PAIRED>
+__global__ void __launch_bounds__(256)
+gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                float* __restrict__ partial) {
+  constexpr int BM = 256, BNL = 256, BK = 64;
+  constexpr int BN_OUT = PAIRED ? 128 : 256;
+  constexpr int STAGE = (BM + BNL) * BK;  // bf16 elements per stage
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE];
+
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN_OUT - 1) / BN_OUT, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave >> 1) * 128, wn0 = (wave & 1) * 128;
+  const int m0 = tile.m * BM, n0 = tile.n * BN_OUT;
+  const int k_begin = tile.split * k_per_split;
+  const int nk = k_per_split / BK;
+
+  // DMA sources: A and B each fill a stage with 32 wave instructions of 1 KB
+  // (8 rows of 128 bytes); wave w issues rows 8 (w + 4 i) .. + 7, i < 8.
+  // Lane l writes slot l % 8 of row l / 8, so it fetches the chunk stored
+  // there.  Rows past M or N are clamped (their results are never stored).
+  uint32_t aoff[8], boff[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = 8 * (wave + 4 * i) + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 3);
+    aoff[i] = (uint32_t)(((int64_t)min(m0 + r, M - 1) * lda + c * 8) * 2);
+    int n;
+    int64_t off = 0;
+    if (PAIRED) {
+      const int grp = r >> 5;
+      n = n0 + (grp >> 1) * 32 + (r & 31);
+      off = (grp & 1) * pair_off;
+    } else {
+      n = n0 + r;
+    }
+    boff[i] = (uint32_t)((off + (int64_t)min(n, N - 1) * ldb + c * 8) * 2);
+  }
+  const char* Ab = reinterpret_cast<const char*>(A + k_begin);
+  const char* Bb = reinterpret_cast<const char*>(B + k_begin);
+  auto issue = [&](int st, int buf) {
+    bf16_t* sa = lds + buf * STAGE;
+    bf16_t* sb = sa + BM * BK;
+    const int kb = st * BK * 2;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_global_load_lds(Ab + kb + aoff[i], sa + (wave + 4 * i) * 512, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(Bb + kb + boff[i], sb + (wave + 4 * i) * 512, 16, 0, 0);
+    }
+  };
+
+  // Fragment reads: lane l holds row l % 32 of a 32-row block, K chunk
+  // 2 q + l / 32 of quarter q.
+  const int fr = lane & 31, fg = lane >> 5;
+  const int sw = (fr & 7) ^ ((fr >> 3) & 3);
+  int foff[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) foff[q] = fr * BK + 8 * ((2 * q + fg) ^ sw);
+  auto read_frags = [&](int buf, int q, bf16x8(&af)[4], bf16x8(&bfr)[4]) {
+    const bf16_t* sa = lds + buf * STAGE + foff[q];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(sa + (wm0 + 32 * i) * BK);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(sa + (BM + wn0 + 32 * j) * BK);
+  };
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  auto mfma = [&](const bf16x8(&af)[4], const bf16x8(&bfr)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  };
+  // a quarter whose eight fragment reads follow its first eight MFMAs
+  auto reads_under_mfma = [] {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Every step issues the DMAs of the step after next; past the last step
+  // the source is clamped to the last step (data never read), which keeps
+  // every wait below the same at each step.
+  issue(0, 0);
+  issue(min(1, nk - 1), 1);
+  SR_VM_BARRIER(16);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
+  bf16x8 a0[4], b0[4], a1[4], b1[4];
+  read_frags(0, 0, a0, b0);
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t & 1;
+    read_frags(buf, 1, a1, b1);
+    mfma(a0, b0);
+    reads_under_mfma();
+    read_frags(buf, 2, a0, b0);
+    mfma(a1, b1);
+    reads_under_mfma();
+    read_frags(buf, 3, a1, b1);
+    mfma(a0, b0);
+    reads_under_mfma();
+    // step t + 1 landed; every wave is done reading buffer `buf`
+    SR_VM_BARRIER(0);
+    __builtin_amdgcn_sched_barrier(0);
+    // (after the last step this reads a stale buffer that is never used)
+    read_frags(buf ^ 1, 0, a0, b0);
+    issue(min(t + 2, nk - 1), buf);
+    mfma(a1, b1);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x010, 2, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // no DMA may still be writing LDS when the work-group ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+  if (!PAIRED && !partial && epi.mode == EPI_RESID) {
+    // residual add: all 64 old values of a row block are loaded before any
+    // store, so their latencies overlap
+    float* h = reinterpret_cast<float*>(epi.out);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float old[4][16];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
+          const int n = n0 + wn0 + j * 32 + fr;
+          old[j][e] = (m < M && n < N) ? h[(int64_t)m * epi.ldo + n] : 0.f;
+        }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
+          const int n = n0 + wn0 + j * 32 + fr;
+          if (m < M && n < N) h[(int64_t)m * epi.ldo + n] = old[j][e] + acc[i][j][e];
+        }
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
+      if (m >= M) continue;
+      if (PAIRED) {
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          const int n = n0 + (wn0 >> 1) + jj * 32 + fr;
+          if (n >= N) continue;
+          const float g = acc[i][2 * jj][e], u = acc[i][2 * jj + 1][e];
+          if (partial) {
+            float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
+            p[n] = g;
+            p[N + n] = u;
+          } else {
+            store_out(epi, m, n, silu(g) * u);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = n0 + wn0 + j * 32 + fr;
+          if (n >= N) continue;
+          if (partial)
+            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
+          else
+            epi_one(epi, m, n, acc[i][j][e]);
+        }
+      }
+    }
+}
+#undef SR_VM_BARRIER
+
+
 // -------------------------------------------- bf16 MFMA GEMM, few rows
 // For M <= 128 (decode after the cuts) the weights dominate: every weight
 // element is used by only M rows.  Work-group = 4 waves over 128 output
@@ -603,12 +816,35 @@ static int skinny_max_rows() {
   return v;
 }
 
+// Rows from which the LDS-DMA 256 x 256 tile is used (from 256 rows also
+// when the tile grid alone fills most of the CUs).
+static int dma_min_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_DMA_MIN_M");
+    return e ? atoi(e) : 1024;
+  }();
+  return v;
+}
+
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
   p.big = false;
   p.skinny = false;
+  p.dma = false;
   if (dtype != SR_BF16) return p;
+  const int64_t dma_tiles = (int64_t)((M + 255) / 256) * ((N + (paired ? 127 : 255)) / (paired ? 128 : 256));
+  if (K % 64 == 0 && (M >= dma_min_rows() || (M >= 256 && dma_tiles >= 192))) {
+    // One work-group per CU at least: split K (each split a multiple of 64
+    // and at least 512 long) while the tile grid is smaller than 256.
+    p.dma = true;
+    const int64_t tiles = dma_tiles;
+    int splits = 1;
+    while (tiles * splits < 256 && K % (splits * 2 * 64) == 0 && K / (splits * 2) >= 512 && splits < 8)
+      splits *= 2;
+    p.splits = splits;
+    return p;
+  }
   if (M >= big_tile_min_rows()) {
     p.big = true;
     return p;
@@ -647,6 +883,14 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     splits *= 2;
   p.splits = splits;
   return p;
+}
+
+// The LDS-DMA kernel addresses its operands with 32-bit byte offsets from the
+// K base of the split.
+static bool dma_offsets_fit(const GemmArgs& g) {
+  const int64_t a = ((int64_t)(g.M - 1) * g.lda + g.K) * 2;
+  const int64_t b = ((g.paired ? g.pair_off : 0) + (int64_t)(g.N - 1) * g.ldb + g.K) * 2;
+  return a < (1LL << 32) && b < (1LL << 32) && g.pair_off >= 0;
 }
 
 int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
@@ -707,7 +951,17 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
 #undef SR_SKINNY_ALL
 #undef SR_SKINNY
     SR_CHECK_LAUNCH();
-  } else if (plan.big) {
+  } else if (plan.dma && dma_offsets_fit(g)) {
+    const int bn_out = g.paired ? 128 : 256;
+    dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
+    if (g.paired)
+      hipLaunchKernelGGL(gemm_dma_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+    else
+      hipLaunchKernelGGL(gemm_dma_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+    SR_CHECK_LAUNCH();
+  } else if (plan.big || plan.dma) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
     if (g.paired)

@@ -31,6 +31,7 @@ struct GemmPlan {
   int splits;
   bool big;     // 256 x 256 tile kernel
   bool skinny;  // weight-streaming kernel for M <= 128
+  bool dma;     // 256 x 256 tile fed by LDS DMA
 };
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired);
 size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired);
