@@ -564,6 +564,151 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 #undef SR_VM_BARRIER
 
 
+// ------------------------------------- bf16 MFMA GEMM, few rows (LDS DMA)
+// For the decode projections (a few hundred rows at most) the weights are
+// streamed once from HBM; what matters is keeping enough of them in flight.
+// Block tile BM x BN (PAIRED: BN gate rows then BN up rows, BN output
+// columns), K step 64, NST LDS stages filled by global_load_lds_dwordx4 up to
+// NST - 1 steps ahead.  LDS stage: the BM activation rows then the weight
+// rows, 128 bytes each, chunk c of row r in slot c ^ (r & 7) ^ ((r >> 3) & 1)
+// (conflict-free 16-byte fragment reads over any 16 consecutive rows).
+// 4 waves in a WGM x WGN grid, each a (BM / WGM) x (BN / WGN) tile of
+// v_mfma_f32_16x16x32_bf16 accumulators.
+#define SR_VMB(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
+// One 16-byte-per-lane memory-to-LDS copy (wave-uniform LDS destination).
+// A plain function, so that kernel templates can call it with dependent
+// arguments.
+__device__ __forceinline__ void dma16(const char* src, bf16_t* lds_dst) {
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+}
+
+template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED>
+__global__ void __launch_bounds__(256)
+gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                   int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                   float* __restrict__ partial) {
+  constexpr int NB = PAIRED ? 2 : 1;
+  constexpr int BNL = NB * BN;                  // weight rows per tile
+  constexpr int ROWS = BM + BNL;
+  constexpr int BK = 64, STAGE = ROWS * BK;     // bf16 elements per stage
+  constexpr int D = ROWS / 32;                  // DMA instructions per wave per stage
+  constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
+  static_assert(ROWS % 32 == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1, "tile shape");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
+
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  const int m0 = tile.m * BM, n0 = tile.n * BN;
+  const int k_begin = tile.split * k_per_split;
+  const int nk = k_per_split / BK;
+
+  // DMA instruction j covers tile rows 8 j .. 8 j + 7 (activation rows
+  // first); wave w issues j = w + 4 q.  Lane l writes slot l % 8 of row
+  // l / 8 and fetches the chunk stored there; rows past M or N are clamped
+  // (their results are never stored).
+  uint32_t off[D];
+#pragma unroll
+  for (int q = 0; q < D; ++q) {
+    const int r = 8 * (wave + 4 * q) + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 1);
+    int64_t e;
+    if (r < BM) {
+      e = (int64_t)min(m0 + r, M - 1) * lda;
+    } else {
+      const int rb = r - BM, blk = rb / BN;
+      e = blk * pair_off + (int64_t)min(n0 + rb - blk * BN, N - 1) * ldb;
+    }
+    off[q] = (uint32_t)((e + c * 8) * 2);
+  }
+  const char* Ab = reinterpret_cast<const char*>(A + k_begin);
+  const char* Bb = reinterpret_cast<const char*>(B + k_begin);
+  auto issue = [&](int st, int buf) {
+    bf16_t* dst = lds + buf * STAGE;
+    const int kb = st * BK * 2;
+#pragma unroll
+    for (int q = 0; q < D; ++q) {
+      const bool is_a = 8 * (wave + 4 * q) < BM;  // wave-uniform
+      dma16((is_a ? Ab : Bb) + kb + off[q], dst + (wave + 4 * q) * 512);
+    }
+  };
+
+  // 16x16x32 fragments: lane l holds row l % 16 of a 16-row block, K chunk
+  // 4 s + l / 16 of sub-step s.
+  const int fr = lane & 15, fg = lane >> 4;
+  const int sw = (fr & 7) ^ ((fr >> 3) & 1);
+  const int foff[2] = {fr * BK + 8 * ((0 + fg) ^ sw), fr * BK + 8 * ((4 + fg) ^ sw)};
+
+  f32x4 acc[NB][TI][TJ];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int st = 0; st < NST - 1; ++st) issue(min(st, nk - 1), st);
+  for (int t = 0; t < nk; ++t) {
+    // step t landed; every wave is done with step t - 1's buffer
+    constexpr int VMN = (NST - 2) * D;
+    static_assert(VMN == 0 || VMN == 8 || VMN == 16 || VMN == 18 || VMN == 20 || VMN == 24, "wait count");
+    if constexpr (VMN == 0) SR_VMB(0);
+    else if constexpr (VMN == 8) SR_VMB(8);
+    else if constexpr (VMN == 16) SR_VMB(16);
+    else if constexpr (VMN == 18) SR_VMB(18);
+    else if constexpr (VMN == 20) SR_VMB(20);
+    else SR_VMB(24);
+    issue(min(t + NST - 1, nk - 1), (t + NST - 1) % NST);
+    const bf16_t* base = lds + (t % NST) * STAGE;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      bf16x8 af[TI], bfr[NB][TJ];
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (wm0 + 16 * i) * BK);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          bfr[b][j] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (BM + b * BN + wn0 + 16 * j) * BK);
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j)
+            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+    }
+  }
+  // no DMA may still be writing LDS when the work-group ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // Accumulator layout: lane holds rows 4*(lane/16) + e, column lane % 16.
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm0 + i * 16 + fg * 4 + e;
+        const int n = n0 + wn0 + j * 16 + fr;
+        if (m >= M || n >= N) continue;
+        if (partial) {
+          const int nout = NB * N;
+          float* p = partial + ((int64_t)tile.split * M + m) * nout;
+          p[n] = acc[0][i][j][e];
+          if (PAIRED) p[N + n] = acc[NB - 1][i][j][e];
+        } else if (PAIRED) {
+          store_out(epi, m, n, silu(acc[0][i][j][e]) * acc[NB - 1][i][j][e]);
+        } else {
+          epi_one(epi, m, n, acc[0][i][j][e]);
+        }
+      }
+}
+#undef SR_VMB
+
 // -------------------------------------------- bf16 MFMA GEMM, few rows
 // For M <= 128 (decode after the cuts) the weights dominate: every weight
 // element is used by only M rows.  Work-group = 4 waves over 128 output
@@ -826,13 +971,37 @@ static int dma_min_rows() {
   return v;
 }
 
+// Rows up to which the LDS-DMA streaming kernel is used.
+static int stream_max_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_STREAM_MAX_M");
+    return e ? atoi(e) : 128;
+  }();
+  return v;
+}
+
+static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
+
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
   p.big = false;
   p.skinny = false;
   p.dma = false;
+  p.stream = 0;
+  p.stream_bn = 0;
   if (dtype != SR_BF16) return p;
+  if (M <= stream_max_rows() && M <= 128 && K % 64 == 0 && (M <= 64 || N <= 65536)) {
+    // One round of work-groups (one per CU): split K by the largest power of
+    // two that keeps the grid within 256 and each split a multiple of 64.
+    p.stream = stream_tile_rows(M);
+    p.stream_bn = 64;
+    const int64_t tiles = (int64_t)((M + p.stream - 1) / p.stream) * ((N + p.stream_bn - 1) / p.stream_bn);
+    int splits = 1;
+    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 64) == 0) splits *= 2;
+    p.splits = splits;
+    return p;
+  }
   const int64_t dma_tiles = (int64_t)((M + 255) / 256) * ((N + (paired ? 127 : 255)) / (paired ? 128 : 256));
   if (K % 64 == 0 && (M >= dma_min_rows() || (M >= 256 && dma_tiles >= 192))) {
     // One work-group per CU at least: split K (each split a multiple of 64
@@ -950,6 +1119,24 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     }
 #undef SR_SKINNY_ALL
 #undef SR_SKINNY
+    SR_CHECK_LAUNCH();
+  } else if (plan.stream && dma_offsets_fit(g)) {
+    dim3 grid = tile_grid((g.M + plan.stream - 1) / plan.stream, (g.N + plan.stream_bn - 1) / plan.stream_bn, splits);
+#define SR_STREAM(BM, BN, WGM, WGN, NST, P)                                                              \
+  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P>), grid, dim3(256), 0, s,               \
+                     (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, \
+                     part)
+    if (plan.stream == 32) {
+      if (g.paired) SR_STREAM(32, 64, 1, 4, 6, true);
+      else SR_STREAM(32, 64, 1, 4, 8, false);
+    } else if (plan.stream == 64) {
+      if (g.paired) SR_STREAM(64, 64, 2, 2, 5, true);
+      else SR_STREAM(64, 64, 2, 2, 7, false);
+    } else {
+      if (g.paired) SR_STREAM(128, 64, 2, 2, 4, true);
+      else SR_STREAM(128, 64, 2, 2, 5, false);
+    }
+#undef SR_STREAM
     SR_CHECK_LAUNCH();
   } else if (plan.dma && dma_offsets_fit(g)) {
     const int bn_out = g.paired ? 128 : 256;
