@@ -253,6 +253,26 @@ sr_status sr_projection(int32_t dtype, const void *x, const void *w, int32_t M, 
                         void *stream);
 size_t sr_projection_scratch(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t mode);
 
+/* Decode attention of `rows` candidates (section a4 of the hot path; the
+ * attention step of the decoder in section 4.2 with the prompt's keys stored
+ * once): for row r and query head j, the single query q[r][j] (DEVICE float
+ * [rows][n_heads][head_dim]) attends the keys/values of KV head
+ * floor(j * n_kv_heads / n_heads): first the shared prefix kpre/vpre (DEVICE
+ * dtype [n_kv_heads][P][head_dim]), then the row's own tail ktail/vtail
+ * (DEVICE dtype [rows][n_kv_heads][cap][head_dim], tokens 0..lt-1 used);
+ * out[r][j*head_dim + d] (DEVICE dtype [rows][n_heads*head_dim]) =
+ * sum_k softmax_k(q . key_k / sqrt(head_dim)) value_k[d].  P + lt >= 1,
+ * lt <= cap, head_dim in {32, 64, 128}, n_heads / n_kv_heads in {1,2,4,8}.
+ * scratch: DEVICE float scratch of >= sr_decode_attention_scratch(...)
+ * floats (split-K partials).  Asynchronous. */
+sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                              int32_t rows, const float *q, const void *kpre, const void *vpre,
+                              int32_t P, const void *ktail, const void *vtail, int32_t cap,
+                              int32_t lt, void *out, float *scratch, size_t scratch_elems,
+                              void *stream);
+size_t sr_decode_attention_scratch(int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                   int32_t rows, int32_t P, int32_t lt);
+
 /* Teacher-forced generator logits through the decode path: all `rows`
  * continue `prompt` (HOST int32 [prompt_len]) with their own tokens
  * (DEVICE int32 [rows][len]); logits_out (DEVICE float [rows][len][vocab])

@@ -82,6 +82,20 @@ def causal_attention(q, k, v, n_kv_heads):
     return o
 
 
+def decode_attention(q, k, v, n_kv_heads):
+    """Attention of one new query per head over a cached sequence (the decode
+    step of section 4.2): q [hq][hd]; k, v [T][hkv][hd], the query being the
+    newest position, so it sees all T keys.  Equals the last row of
+    ``causal_attention`` over the same keys."""
+    hq, hd = q.shape
+    o = np.empty_like(q)
+    for j in range(hq):
+        kh = (j * n_kv_heads) // hq
+        sc = (k[:, kh, :] @ q[j]) / np.sqrt(hd)
+        o[j] = softmax(sc) @ v[:, kh, :]
+    return o
+
+
 class Transformer:
     """A decoder given by a shape (see ``synth.ModelShape``) and weights."""
 

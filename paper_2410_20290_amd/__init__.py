@@ -101,7 +101,11 @@ def lib():
         L.sr_projection.argtypes = [_i32, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, ctypes.c_size_t, _vp]
         L.sr_projection_scratch.argtypes = [_i32, _i32, _i32, _i32, _i32]
         L.sr_projection_scratch.restype = ctypes.c_size_t
-        for f in ("sr_projection", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
+        L.sr_decode_attention.argtypes = [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _i32, _i32,
+                                          _vp, _vp, ctypes.c_size_t, _vp]
+        L.sr_decode_attention_scratch.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32]
+        L.sr_decode_attention_scratch.restype = ctypes.c_size_t
+        for f in ("sr_projection", "sr_decode_attention", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
                   "sr_logits_teacher_forced", "sr_reward_scores"):
             getattr(L, f).restype = _i32
         _lib = L
@@ -252,6 +256,22 @@ def projection(x, w, mode: int, out, stream=None):
     part = torch.empty(max(need, 1), dtype=torch.float32, device=x.device)
     _check(lib().sr_projection(dtype, _ptr(x), _ptr(w), M, N, K, mode, _ptr(out), _ptr(part), need,
                                _stream(stream)))
+    return part
+
+
+def decode_attention(q, kpre, vpre, ktail, vtail, lt: int, out, stream=None):
+    """sr_decode_attention: q float [rows][hq][hd]; kpre/vpre [hkv][P][hd]
+    (or None when P = 0); ktail/vtail [rows][hkv][cap][hd]; out [rows][hq*hd]
+    in the model dtype (bf16 tensors travel as int16).  See the header."""
+    import torch
+    rows, hq, hd = q.shape
+    hkv, cap = ktail.shape[1], ktail.shape[2]
+    P = 0 if kpre is None else kpre.shape[1]
+    dtype = SR_BF16 if ktail.dtype in (torch.int16, torch.bfloat16) else SR_F32
+    need = int(lib().sr_decode_attention_scratch(hd, hq, hkv, rows, P, lt))
+    part = torch.empty(max(need, 1), dtype=torch.float32, device=q.device)
+    _check(lib().sr_decode_attention(dtype, hd, hq, hkv, rows, _ptr(q), _ptr(kpre), _ptr(vpre), P, _ptr(ktail),
+                                     _ptr(vtail), cap, lt, _ptr(out), _ptr(part), need, _stream(stream)))
     return part
 
 

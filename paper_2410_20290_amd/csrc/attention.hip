@@ -11,6 +11,9 @@
 // Prefill (reward-model scoring, prompt): a work-group owns a block of
 // queries of one row and one KV head; K/V tiles are staged in LDS as fp32
 // and shared by all its queries.
+#include <algorithm>
+#include <cstdlib>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -19,6 +22,31 @@ namespace sr {
 constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float exp2_or_zero(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
+
+// DPP move within rows of 16 lanes (ctrl: quad_perm 0x00-0xff, row_mirror
+// 0x140, row_half_mirror 0x141).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over aligned groups of LPK lanes; every lane of a group gets the sum.
+// Groups of 16 use DPP within the row (xor 1, xor 2, then the mirrored
+// quad and half), wider groups cross-lane shuffles.
+template <int LPK>
+__device__ __forceinline__ float group_sum(float d) {
+  if constexpr (LPK == 16) {
+    d += dpp_f32<0xB1>(d);   // quad_perm [1,0,3,2]
+    d += dpp_f32<0x4E>(d);   // quad_perm [2,3,0,1]
+    d += dpp_f32<0x141>(d);  // row_half_mirror
+    d += dpp_f32<0x140>(d);  // row_mirror
+    return d;
+  } else {
+#pragma unroll
+    for (int o = LPK / 2; o > 0; o >>= 1) d += __shfl_xor(d, o, 64);
+    return d;
+  }
+}
 
 template <typename T, int HD, int G>
 __global__ void __launch_bounds__(256)
@@ -86,8 +114,7 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
         float d = 0.f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) d = fmaf(qv[g][e], kf[e], d);
-#pragma unroll
-        for (int o = LPK / 2; o > 0; o >>= 1) d += __shfl_xor(d, o, 64);
+        d = group_sum<LPK>(d);
         s[u][g] = valid[u] ? d : -INFINITY;
       }
     }
@@ -189,6 +216,162 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
   }
 }
 
+// Decode attention over keys [key0, P + lt) for bf16, head_dim 128, on
+// MFMA.  Work-group = (split, KV head, row), 4 waves; the G query heads of
+// the KV head are the 16 columns of v_mfma_f32_16x16x32_bf16 (columns >= G
+// are zero queries whose results are dropped).  Stage = 64 keys of K and V
+// (32 KB) copied into LDS with global_load_lds_dwordx4, one stage ahead.
+// Per 32 keys every wave computes
+//   S^T = K Q^T   (two 16-key tiles): lane l holds keys 4(l/16)+i and
+//                 16+4(l/16)+i of query l%16 (all waves alike),
+// the online-softmax update (maximum over the four lane groups), and
+//   O^T += V^T P^T for its own 32 of the 128 dimensions, with the key order
+//                 of the contraction permuted so that the B operand is the
+//                 lane's own 8 probabilities; the A operand reads V at those
+//                 keys (2-byte LDS reads of one dimension).
+// LDS rows of 256 bytes (16 chunks of 8 dims): K chunk c of key k sits in
+// slot c ^ (k & 15), V chunk c in slot c ^ 2 ((k >> 2) & 3), so both read
+// patterns are free of bank conflicts.
+template <int G>
+__global__ void __launch_bounds__(256)
+decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
+                        int P, const bf16_t* __restrict__ ktail, const bf16_t* __restrict__ vtail, int cap, int lt,
+                        int hq, int hkv, int kps, int splits, float* __restrict__ part, bf16_t* __restrict__ out,
+                        float qscale, int key0, int split0) {
+  constexpr int HD = 128, SK = 64, NST = 2;
+  constexpr int STAGE = 2 * SK * HD;  // bf16 elements: K rows then V rows
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
+  const int split = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const int total = P + lt;
+  const int k0 = key0 + split * kps, k1 = min(total, k0 + kps);
+  const int nst = (k1 - k0 + SK - 1) / SK;
+
+  // DMA: a stage is 32 instructions of 4 key rows (1 KB); wave w issues K
+  // rows 4 (w + 4 i) .. + 3, i < 4, and the same V rows.  Lane l writes slot
+  // l % 16 of row l / 16 and fetches the chunk stored there.
+  const bf16_t* kt = ktail + ((int64_t)row * hkv + h) * cap * HD;
+  const bf16_t* vt = vtail + ((int64_t)row * hkv + h) * cap * HD;
+  const bf16_t* kp = kpre + (int64_t)h * P * HD;
+  const bf16_t* vp = vpre + (int64_t)h * P * HD;
+  auto issue = [&](int st, int buf) {
+    bf16_t* dst = lds + buf * STAGE;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int kr = 4 * (wave + 4 * i) + fg;  // key row in the stage
+      const int j = min(k0 + min(st, nst - 1) * SK + kr, k1 - 1);
+      const int64_t rowoff = (int64_t)(j < P ? j : j - P) * HD;
+      const int ck = fr ^ (kr & 15), cv = fr ^ (2 * ((kr >> 2) & 3));
+      dma16(reinterpret_cast<const char*>((j < P ? kp : kt) + rowoff + ck * 8), dst + (wave + 4 * i) * 512);
+      dma16(reinterpret_cast<const char*>((j < P ? vp : vt) + rowoff + cv * 8), dst + SK * HD + (wave + 4 * i) * 512);
+    }
+  };
+
+  // Q^T fragments (B operand): lane holds Q[query fr][32 s + 8 fg .. + 8], scaled, bf16
+  bf16x8 qf[4];
+  {
+    const bool qvalid = fr < G;
+    const float* qr = q + ((int64_t)row * hq + h * G + (qvalid ? fr : 0)) * HD;
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)(qvalid ? qr[32 * s + 8 * fg + e] * qscale : 0.f);
+  }
+  f32x4 o[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  float m = -INFINITY, l = 0.f;
+  // V^T reads: dimension 32 wave + 16 dt + fr, keys 4 fg + i (+ 16)
+  const int vdim0 = 32 * wave + fr;
+
+  issue(0, 0);
+  for (int t = 0; t < nst; ++t) {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    issue(t + 1, (t + 1) & 1);
+    const bf16_t* ks = lds + (t & 1) * STAGE;
+    const bf16_t* vs = ks + SK * HD;
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp) {
+      f32x4 st[2];
+#pragma unroll
+      for (int kt2 = 0; kt2 < 2; ++kt2) {
+        const int key = 32 * tp + 16 * kt2 + fr;
+        st[kt2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + 8 * ((4 * s + fg) ^ (key & 15)));
+          st[kt2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[kt2], 0, 0, 0);
+        }
+      }
+      // this lane's 8 keys: 4 fg + i and 16 + 4 fg + i of the 32
+      float sv[8];
+      const int jb = k0 + t * SK + 32 * tp + 4 * fg;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sv[i] = jb + i < k1 ? st[0][i] : -INFINITY;
+        sv[4 + i] = jb + 16 + i < k1 ? st[1][i] : -INFINITY;
+      }
+      float mt = sv[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sv[i]);
+      mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float mn = fmaxf(m, mt);
+      const bool none = mn == -INFINITY;
+      const float corr = none ? 1.f : exp2f(m - mn);
+      bf16x8 pf;
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float p = none ? 0.f : exp2f(sv[i] - mn);
+        ps += p;
+        pf[i] = (__bf16)p;
+      }
+      l = l * corr + ps;
+      m = mn;
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt) {
+        const int dim = vdim0 + 16 * dt;
+        const int dc = dim >> 3, de = dim & 7;
+        bf16x8 vf;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int key = 32 * tp + 4 * fg + (i & 3) + 16 * (i >> 2);
+          vf[i] = __builtin_bit_cast(__bf16, vs[key * HD + 8 * (dc ^ (2 * ((key >> 2) & 3))) + de]);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[dt][e] *= corr;
+        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[dt], 0, 0, 0);
+      }
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // the row sum over the four lane groups; lane l now holds O^T[dims
+  // 32 w + 16 dt + 4 fg + e][query fr]
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (fr < G) {
+    const int qh = h * G + fr;
+#pragma unroll
+    for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int dim = 32 * wave + 16 * dt + 4 * fg + e;
+        if (splits == 1) {
+          out[((int64_t)row * hq + qh) * HD + dim] = f32_to_bf16(o[dt][e] / l);
+        } else {
+          float* pp = part + (((int64_t)row * hq + qh) * splits + split0 + split) * (HD + 2);
+          pp[dim] = o[dt][e];
+          if (wave == 0 && dt == 0 && fg == 0 && e == 0) {
+            pp[HD] = m;
+            pp[HD + 1] = l;
+          }
+        }
+      }
+  }
+}
+
 template <typename T, int HD>
 __global__ void decode_merge_kernel(const float* __restrict__ part, int splits, int hq,
                                     T* __restrict__ out) {
@@ -216,6 +399,15 @@ static int decode_kps(int rows, int hkv, int keys) {
   return (keys + splits - 1) / splits;
 }
 
+// Keys per split for the MFMA streaming kernel: about two work-groups per
+// CU, at least 64 keys per split.
+static int tail_mfma_kps(int rows, int hkv, int keys) {
+  const int64_t groups = (int64_t)rows * hkv;
+  int splits = (int)std::max<int64_t>(1, (512 + groups - 1) / groups);
+  splits = std::max(1, std::min(splits, keys / 64));
+  return (keys + splits - 1) / splits;
+}
+
 template <int G, bool PREFIX_ONLY>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
@@ -224,23 +416,80 @@ __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16
                                          int part_splits);
 
 // Whether the shared prefix is attended by the batched MFMA kernel.
-static bool prefix_by_mfma(int dtype, int hd, int P) { return dtype == SR_BF16 && hd == 128 && P > 0; }
+static int prefix_mfma_min_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_PREFIX_MFMA_MIN_ROWS");
+    return e ? atoi(e) : 128;
+  }();
+  return v;
+}
+static bool prefix_by_mfma(int dtype, int hd, int P, int rows) {
+  return dtype == SR_BF16 && hd == 128 && P > 0 && rows >= prefix_mfma_min_rows();
+}
 
 // Partial slots needed for `keys` = prefix + maximal tail (upper bound for
 // both the combined and the split-prefix forms).
 int decode_attn_splits(int rows, int hkv, int keys) {
   int kps = decode_kps(rows, hkv, keys);
-  return (keys + kps - 1) / kps + (keys + 63) / 64;
+  const int old_form = (keys + kps - 1) / kps + (keys + 63) / 64;
+  const int dma_form = keys > 0 ? (keys + tail_mfma_kps(rows, hkv, keys) - 1) / tail_mfma_kps(rows, hkv, keys) : 0;
+  return std::max(old_form, dma_form + (keys + 63) / 64);
+}
+
+// Whether the MFMA streaming kernel takes the keys (bf16, head_dim 128, up to
+// 16 query heads per KV head, few rows).
+static bool tail_by_mfma(int dtype, int hd, int g, int rows) {
+  static const int max_rows = [] {
+    const char* e = getenv("SPECREJ_TAIL_MFMA_MAX_ROWS");
+    return e ? atoi(e) : 128;
+  }();
+  return dtype == SR_BF16 && hd == 128 && g <= 16 && rows <= max_rows;
+}
+
+template <int G>
+static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsplit, int splits, int split0,
+                             float qscale, hipStream_t s) {
+  hipLaunchKernelGGL((decode_tail_mfma_kernel<G>), dim3(nsplit, a.hkv, a.rows), dim3(256), 0, s, a.q,
+                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.ktail,
+                     (const bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out,
+                     qscale, key0, split0);
+  SR_CHECK_LAUNCH();
 }
 
 template <typename T, int HD, int G>
 static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
-  if (prefix_by_mfma(a.dtype, HD, a.P)) {
+  if (tail_by_mfma(a.dtype, HD, G, a.rows)) {
+    // optional batched MFMA pass over the shared prefix (slots 0..psplits-1),
+    // then the streaming kernel over the remaining keys, then the merge
+    const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
+    const int psplits = pre ? (a.P + 63) / 64 : 0;
+    const int key0 = pre ? a.P : 0;
+    const int keys = a.P + a.lt - key0;
+    const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
+    const int tsplits = (keys + kps - 1) / kps;
+    const int splits = tsplits + psplits;
+    if (splits > 1)
+      SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
+    if (pre) {
+      hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits),
+                         dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr,
+                         nullptr, a.rows, a.hq, a.hkv, nullptr, qscale, a.part, splits);
+      SR_CHECK_LAUNCH();
+    }
+    if (tsplits > 0) launch_tail_mfma<G>(a, key0, kps, tsplits, splits, psplits, qscale, s);
+    if (splits > 1) {
+      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, splits, a.hq,
+                         (T*)a.out);
+      SR_CHECK_LAUNCH();
+    }
+    return;
+  }
+  if (prefix_by_mfma(a.dtype, HD, a.P, a.rows)) {
     // prefix partials (slots 0..psplits-1, 64 keys each, 16 rows per
     // work-group), then the tail partials
     const int psplits = (a.P + 63) / 64;
-    const int tkps = decode_kps(a.rows, a.hkv, a.lt);
+    const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;
     const int tsplits = (a.lt + tkps - 1) / tkps;
     const int splits = tsplits + psplits;
     SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
@@ -248,10 +497,12 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
                        0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows,
                        a.hq, a.hkv, nullptr, qscale, a.part, splits);
     SR_CHECK_LAUNCH();
-    hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
-                       (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail, (const T*)a.vtail, a.cap, a.lt,
-                       a.hq, a.hkv, tkps, splits, a.part, (T*)a.out, qscale, a.P, psplits);
-    SR_CHECK_LAUNCH();
+    if (tsplits > 0) {
+      hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
+                         (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail, (const T*)a.vtail, a.cap,
+                         a.lt, a.hq, a.hkv, tkps, splits, a.part, (T*)a.out, qscale, a.P, psplits);
+      SR_CHECK_LAUNCH();
+    }
     hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, splits, a.hq,
                        (T*)a.out);
     SR_CHECK_LAUNCH();

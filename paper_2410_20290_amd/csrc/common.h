@@ -56,6 +56,15 @@ template <> struct Vec16<float> {
   }
 };
 
+// One 16-byte-per-lane copy from memory straight into LDS
+// (global_load_lds_dwordx4): lane l's 16 bytes land at lds_dst + 16 l bytes;
+// lds_dst must be the same in every lane of the wave.  Counted by vmcnt.  A
+// plain function, so that kernel templates can call it with dependent
+// arguments.
+__device__ __forceinline__ void dma16(const char* src, bf16_t* lds_dst) {
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+}
+
 // ---- wavefront reductions (64 lanes) ---------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

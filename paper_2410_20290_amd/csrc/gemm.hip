@@ -575,12 +575,6 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // 4 waves in a WGM x WGN grid, each a (BM / WGM) x (BN / WGN) tile of
 // v_mfma_f32_16x16x32_bf16 accumulators.
 #define SR_VMB(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
-// One 16-byte-per-lane memory-to-LDS copy (wave-uniform LDS destination).
-// A plain function, so that kernel templates can call it with dependent
-// arguments.
-__device__ __forceinline__ void dma16(const char* src, bf16_t* lds_dst) {
-  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
-}
 
 template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED>
 __global__ void __launch_bounds__(256)

@@ -1034,6 +1034,39 @@ sr_status sr_projection(int32_t dtype, const void* x, const void* w, int32_t M, 
   });
 }
 
+size_t sr_decode_attention_scratch(int32_t head_dim, int32_t n_heads, int32_t n_kv_heads, int32_t rows, int32_t P,
+                                   int32_t lt) {
+  if (head_dim <= 0 || n_heads <= 0 || n_kv_heads <= 0 || rows <= 0 || P < 0 || lt < 0) return 0;
+  return (size_t)rows * n_heads * decode_attn_splits(rows, n_kv_heads, P + lt) * (head_dim + 2);
+}
+
+sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads, int32_t rows,
+                              const float* q, const void* kpre, const void* vpre, int32_t P, const void* ktail,
+                              const void* vtail, int32_t cap, int32_t lt, void* out, float* scratch,
+                              size_t scratch_elems, void* stream) {
+  return guard([&] {
+    SR_REQUIRE(dtype == SR_F32 || dtype == SR_BF16, SR_ERR_INVALID_ARG, "unknown dtype");
+    SR_REQUIRE(head_dim == 32 || head_dim == 64 || head_dim == 128, SR_ERR_UNSUPPORTED,
+               "head_dim must be 32, 64 or 128");
+    SR_REQUIRE(n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0, SR_ERR_INVALID_ARG, "bad head counts");
+    const int g = n_heads / n_kv_heads;
+    SR_REQUIRE(g == 1 || g == 2 || g == 4 || g == 8, SR_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8");
+    SR_REQUIRE(rows >= 0 && P >= 0 && lt >= 0 && lt <= cap && (rows == 0 || P + lt >= 1), SR_ERR_INVALID_ARG,
+               "bad rows / P / lt / cap");
+    if (rows == 0) return;
+    SR_REQUIRE(q && out && (P == 0 || (kpre && vpre)) && (lt == 0 || (ktail && vtail)), SR_ERR_INVALID_ARG,
+               "NULL buffer");
+    const size_t need = sr_decode_attention_scratch(head_dim, n_heads, n_kv_heads, rows, P, lt);
+    SR_REQUIRE(scratch && scratch_elems >= need, SR_ERR_WORKSPACE_TOO_SMALL,
+               "attention scratch too small: need " + std::to_string(need) + " floats");
+    DecodeAttnArgs a;
+    a.dtype = dtype; a.hd = head_dim; a.hq = n_heads; a.hkv = n_kv_heads; a.rows = rows; a.q = q;
+    a.kpre = kpre; a.vpre = vpre; a.P = P; a.ktail = ktail; a.vtail = vtail; a.cap = cap; a.lt = lt;
+    a.out = out; a.part = scratch; a.part_cap = scratch_elems;
+    decode_attn(a, (hipStream_t)stream);
+  });
+}
+
 sr_status sr_logits_teacher_forced(const sr_model* gen, const sr_model* rm, const int32_t* prompt,
                                    int32_t prompt_len, const sr_params* p, const int32_t* tokens, int32_t rows,
                                    int32_t len, float* logits_out, void* workspace, size_t ws_bytes,

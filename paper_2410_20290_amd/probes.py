@@ -6,6 +6,9 @@
         21 rows, three launches each; prints the algorithmic bytes of each.
     python3 <repo>/paper_2410_20290_amd/probes.py gemm [rows,rows,...]
         Graph-replay timing of the projections at the given row counts.
+    python3 <repo>/paper_2410_20290_amd/probes.py attn
+        Timing of decode attention at the row counts and tail lengths of the
+        three rounds of the 8B-shaped run.
 """
 import json
 import os
@@ -92,8 +95,50 @@ def gemm(rows):
                               "GBs": round(by / t / 1e9)}), flush=True)
 
 
+def attn(cases):
+    """Graph-replay timing of decode attention at (rows, tail length) cases
+    of the 8B shape (prefix 256)."""
+    import torch
+    import paper_2410_20290_amd as sr
+
+    def gtime(f, reps=10):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            f()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                f()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    hq, hkv, hd, P = 32, 8, 128, 256
+    for rows, lt in cases:
+        cap = lt
+        q = torch.randn(rows, hq, hd, device="cuda")
+        kp = (torch.randn(hkv, P, hd, device="cuda") * 0.5).to(torch.bfloat16).view(torch.int16)
+        vp = torch.randn(hkv, P, hd, device="cuda").to(torch.bfloat16).view(torch.int16)
+        kt = (torch.randn(rows, hkv, cap, hd, device="cuda") * 0.5).to(torch.bfloat16).view(torch.int16)
+        vt = torch.randn(rows, hkv, cap, hd, device="cuda").to(torch.bfloat16).view(torch.int16)
+        out = torch.empty(rows, hq * hd, device="cuda", dtype=torch.int16)
+        t = gtime(lambda: sr.decode_attention(q, kp, vp, kt, vt, lt, out))
+        by = 2 * hkv * hd * 2 * (P + rows * lt) + rows * hq * hd * (4 + 2)
+        print(json.dumps({"rows": rows, "lt": lt, "us": round(t * 1e6, 1), "GBs": round(by / t / 1e9)}), flush=True)
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "traffic":
         traffic()
+    elif sys.argv[1] == "attn":
+        attn([(512, 64), (512, 128), (103, 200), (103, 400), (103, 630), (21, 650), (21, 850), (21, 1020)])
     else:
         gemm([int(v) for v in (sys.argv[2] if len(sys.argv) > 2 else "21,103,512,4096,32768").split(",")])

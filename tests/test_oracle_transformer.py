@@ -14,7 +14,7 @@ import pytest
 import torch
 
 import synth
-from oracle.transformer import Transformer, causal_attention, rmsnorm, rope, rope_cos_sin, widen
+from oracle.transformer import Transformer, causal_attention, decode_attention, rmsnorm, rope, rope_cos_sin, widen
 
 transformers = pytest.importorskip("transformers")
 
@@ -141,3 +141,18 @@ def test_causal_gqa_attention_matches_torch_sdpa(hq, hkv):
         torch.from_numpy(q.transpose(1, 0, 2))[None], torch.from_numpy(k.transpose(1, 0, 2))[None],
         torch.from_numpy(v.transpose(1, 0, 2))[None], is_causal=True, enable_gqa=True)[0].numpy()
     assert np.abs(causal_attention(q, k, v, hkv) - ref.transpose(1, 0, 2)).max() < 1e-12
+
+
+@pytest.mark.parametrize("hq,hkv,T", [(4, 4, 1), (8, 2, 9), (32, 8, 40)])
+def test_decode_attention_is_last_causal_row_and_sdpa(hq, hkv, T):
+    """One new query over a cached sequence: the last row of causal
+    attention, and torch's (non-causal) SDPA of that single query."""
+    rng = np.random.default_rng(hq + 100 * T)
+    hd = 16
+    q, k, v = rng.normal(size=(T, hq, hd)), rng.normal(size=(T, hkv, hd)), rng.normal(size=(T, hkv, hd))
+    got = decode_attention(q[-1], k, v, hkv)
+    assert np.abs(got - causal_attention(q, k, v, hkv)[-1]).max() < 1e-12
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q[-1:].transpose(1, 0, 2))[None], torch.from_numpy(k.transpose(1, 0, 2))[None],
+        torch.from_numpy(v.transpose(1, 0, 2))[None], enable_gqa=True)[0].numpy()
+    assert np.abs(got - ref[:, 0, :]).max() < 1e-12
