@@ -566,14 +566,15 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 
 // ------------------------------------- bf16 MFMA GEMM, few rows (LDS DMA)
 // For the decode projections (a few hundred rows at most) the weights are
-// streamed once from HBM; what matters is keeping enough of them in flight.
-// Block tile BM x BN (PAIRED: BN gate rows then BN up rows, BN output
-// columns), K step 64, NST LDS stages filled by global_load_lds_dwordx4 up to
-// NST - 1 steps ahead.  LDS stage: the BM activation rows then the weight
-// rows, 128 bytes each, chunk c of row r in slot c ^ (r & 7) ^ ((r >> 3) & 1)
-// (conflict-free 16-byte fragment reads over any 16 consecutive rows).
-// 4 waves in a WGM x WGN grid, each a (BM / WGM) x (BN / WGN) tile of
-// v_mfma_f32_16x16x32_bf16 accumulators.
+// streamed once from HBM; what matters is keeping enough of them in flight
+// and keeping the per-step overhead small.  Block tile BM x BN (PAIRED: BN
+// gate rows then BN up rows, BN output columns), K step 128, NST LDS stages
+// filled by global_load_lds_dwordx4 up to NST - 1 steps ahead, one barrier
+// per step.  LDS stage: the BM activation rows then the weight rows, 256
+// bytes each, 16-byte chunk c of row r in slot c ^ (r & 15) (conflict-free
+// fragment reads).  4 waves in a WGM x WGN grid, each a (BM / WGM) x
+// (BN / WGN) tile of v_mfma_f32_16x16x32_bf16 accumulators; the fragment
+// reads of the next 32-wide sub-step run under the MFMAs of the current one.
 #define SR_VMB(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
 template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED>
@@ -584,10 +585,10 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   constexpr int NB = PAIRED ? 2 : 1;
   constexpr int BNL = NB * BN;                  // weight rows per tile
   constexpr int ROWS = BM + BNL;
-  constexpr int BK = 64, STAGE = ROWS * BK;     // bf16 elements per stage
-  constexpr int D = ROWS / 32;                  // DMA instructions per wave per stage
+  constexpr int BK = 128, STAGE = ROWS * BK;    // bf16 elements per stage
+  constexpr int D = ROWS / 16;                  // DMA instructions per wave per stage
   constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
-  static_assert(ROWS % 32 == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1, "tile shape");
+  static_assert(ROWS % 16 == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1, "tile shape");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
 
   const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, K / k_per_split);
@@ -599,15 +600,15 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   const int k_begin = tile.split * k_per_split;
   const int nk = k_per_split / BK;
 
-  // DMA instruction j covers tile rows 8 j .. 8 j + 7 (activation rows
-  // first); wave w issues j = w + 4 q.  Lane l writes slot l % 8 of row
-  // l / 8 and fetches the chunk stored there; rows past M or N are clamped
+  // DMA instruction j covers tile rows 4 j .. 4 j + 3 (activation rows
+  // first); wave w issues j = w + 4 q.  Lane l writes slot l % 16 of row
+  // l / 16 and fetches the chunk stored there; rows past M or N are clamped
   // (their results are never stored).
   uint32_t off[D];
 #pragma unroll
   for (int q = 0; q < D; ++q) {
-    const int r = 8 * (wave + 4 * q) + (lane >> 3);
-    const int c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 1);
+    const int r = 4 * (wave + 4 * q) + (lane >> 4);
+    const int c = (lane & 15) ^ (r & 15);
     int64_t e;
     if (r < BM) {
       e = (int64_t)min(m0 + r, M - 1) * lda;
@@ -624,16 +625,17 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     const int kb = st * BK * 2;
 #pragma unroll
     for (int q = 0; q < D; ++q) {
-      const bool is_a = 8 * (wave + 4 * q) < BM;  // wave-uniform
+      const bool is_a = 4 * (wave + 4 * q) < BM;  // wave-uniform
       dma16((is_a ? Ab : Bb) + kb + off[q], dst + (wave + 4 * q) * 512);
     }
   };
 
   // 16x16x32 fragments: lane l holds row l % 16 of a 16-row block, K chunk
-  // 4 s + l / 16 of sub-step s.
+  // 4 s + l / 16 of sub-step s (s < 4), stored in slot chunk ^ (l % 16).
   const int fr = lane & 15, fg = lane >> 4;
-  const int sw = (fr & 7) ^ ((fr >> 3) & 1);
-  const int foff[2] = {fr * BK + 8 * ((0 + fg) ^ sw), fr * BK + 8 * ((4 + fg) ^ sw)};
+  int foff[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) foff[s] = fr * BK + 8 * ((4 * s + fg) ^ fr);
 
   f32x4 acc[NB][TI][TJ];
 #pragma unroll
@@ -642,39 +644,66 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     for (int i = 0; i < TI; ++i)
 #pragma unroll
       for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto read_frags = [&](const bf16_t* base, int s, bf16x8(&af)[TI], bf16x8(&bfr)[NB][TJ]) {
+#pragma unroll
+    for (int i = 0; i < TI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (wm0 + 16 * i) * BK);
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        bfr[b][j] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (BM + b * BN + wn0 + 16 * j) * BK);
+  };
+  auto mfma = [&](const bf16x8(&af)[TI], const bf16x8(&bfr)[NB][TJ]) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+  };
+
+  // one MFMA, then one fragment read of the next sub-step, alternating;
+  // then the remaining MFMAs
+  constexpr int NMF = NB * TI * TJ, NRD = TI + NB * TJ;
+  auto interleave = [] {
+#pragma unroll
+    for (int k = 0; k < (NRD < NMF ? NRD : NMF); ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (NRD > NMF) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NMF, 0);
+    if constexpr (NMF > NRD) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
   for (int st = 0; st < NST - 1; ++st) issue(min(st, nk - 1), st);
   for (int t = 0; t < nk; ++t) {
     // step t landed; every wave is done with step t - 1's buffer
     constexpr int VMN = (NST - 2) * D;
-    static_assert(VMN == 0 || VMN == 8 || VMN == 16 || VMN == 18 || VMN == 20 || VMN == 24, "wait count");
+    static_assert(VMN == 0 || VMN == 10 || VMN == 12 || VMN == 16 || VMN == 18 || VMN == 24, "wait count");
     if constexpr (VMN == 0) SR_VMB(0);
-    else if constexpr (VMN == 8) SR_VMB(8);
+    else if constexpr (VMN == 10) SR_VMB(10);
+    else if constexpr (VMN == 12) SR_VMB(12);
     else if constexpr (VMN == 16) SR_VMB(16);
     else if constexpr (VMN == 18) SR_VMB(18);
-    else if constexpr (VMN == 20) SR_VMB(20);
     else SR_VMB(24);
     issue(min(t + NST - 1, nk - 1), (t + NST - 1) % NST);
     const bf16_t* base = lds + (t % NST) * STAGE;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      bf16x8 af[TI], bfr[NB][TJ];
-#pragma unroll
-      for (int i = 0; i < TI; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (wm0 + 16 * i) * BK);
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-          bfr[b][j] = *reinterpret_cast<const bf16x8*>(base + foff[s] + (BM + b * BN + wn0 + 16 * j) * BK);
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int i = 0; i < TI; ++i)
-#pragma unroll
-          for (int j = 0; j < TJ; ++j)
-            acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
-    }
+    bf16x8 a0[TI], b0[NB][TJ], a1[TI], b1[NB][TJ];
+    read_frags(base, 0, a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+    read_frags(base, 1, a1, b1);
+    mfma(a0, b0);
+    interleave();
+    read_frags(base, 2, a0, b0);
+    mfma(a1, b1);
+    interleave();
+    read_frags(base, 3, a1, b1);
+    mfma(a0, b0);
+    interleave();
+    mfma(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
   }
   // no DMA may still be writing LDS when the work-group ends
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -985,14 +1014,14 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.stream = 0;
   p.stream_bn = 0;
   if (dtype != SR_BF16) return p;
-  if (M <= stream_max_rows() && M <= 128 && K % 64 == 0 && (M <= 64 || N <= 65536)) {
+  if (M <= stream_max_rows() && M <= 128 && K % 128 == 0 && (M <= 64 || N <= 65536)) {
     // One round of work-groups (one per CU): split K by the largest power of
-    // two that keeps the grid within 256 and each split a multiple of 64.
+    // two that keeps the grid within 256 and each split a multiple of 128.
     p.stream = stream_tile_rows(M);
     p.stream_bn = 64;
     const int64_t tiles = (int64_t)((M + p.stream - 1) / p.stream) * ((N + p.stream_bn - 1) / p.stream_bn);
     int splits = 1;
-    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 64) == 0) splits *= 2;
+    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 128) == 0) splits *= 2;
     p.splits = splits;
     return p;
   }
@@ -1121,14 +1150,14 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, \
                      part)
     if (plan.stream == 32) {
-      if (g.paired) SR_STREAM(32, 64, 1, 4, 6, true);
-      else SR_STREAM(32, 64, 1, 4, 8, false);
+      if (g.paired) SR_STREAM(32, 64, 1, 4, 3, true);
+      else SR_STREAM(32, 64, 1, 4, 5, false);
     } else if (plan.stream == 64) {
-      if (g.paired) SR_STREAM(64, 64, 2, 2, 5, true);
-      else SR_STREAM(64, 64, 2, 2, 7, false);
+      if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true);
+      else SR_STREAM(64, 64, 2, 2, 4, false);
     } else {
-      if (g.paired) SR_STREAM(128, 64, 2, 2, 4, true);
-      else SR_STREAM(128, 64, 2, 2, 5, false);
+      if (g.paired) SR_STREAM(128, 64, 2, 2, 2, true);
+      else SR_STREAM(128, 64, 2, 2, 3, false);
     }
 #undef SR_STREAM
     SR_CHECK_LAUNCH();
