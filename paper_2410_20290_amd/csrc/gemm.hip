@@ -1014,7 +1014,7 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.stream = 0;
   p.stream_bn = 0;
   if (dtype != SR_BF16) return p;
-  if (M <= stream_max_rows() && M <= 128 && K % 128 == 0 && (M <= 64 || N <= 65536)) {
+  if (M <= stream_max_rows() && K % 128 == 0 && (M <= 64 || N <= 65536)) {
     // One round of work-groups (one per CU): split K by the largest power of
     // two that keeps the grid within 256 and each split a multiple of 128.
     p.stream = stream_tile_rows(M);

@@ -64,8 +64,16 @@ __device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int o) {
 }
 
 constexpr int kSampleThreads = 1024;
-constexpr int kMaxSegments = 4096;  // vocab <= 262144
+constexpr int kPerLane = 8;                       // consecutive elements per lane and step
+constexpr int kSegment = 64 * kPerLane;           // elements per segment (one wave step)
+constexpr int kMaxSegments = kSampleThreads;      // vocab <= 524288
 
+// One work-group per row.  Pass 1: maximum and its first index.  Pass 2:
+// exact integer weights, summed per segment of 512 consecutive entries (a
+// wave step: 8 consecutive entries per lane, one wave reduction).  Block
+// scan of the segment sums, the segment holding the drawn point, then
+// wave 0 finds the lane and the lane its entry.  All sums are exact 64-bit
+// integers, so the drawn token does not depend on the grouping.
 __global__ void __launch_bounds__(kSampleThreads)
 sample_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab,
               const int32_t* __restrict__ cand, int step, float inv_t, int greedy, uint2 key,
@@ -88,12 +96,38 @@ sample_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab,
     found_base = 0;
   }
 
-  // pass 1: maximum (and its first index, for greedy decoding)
+  // 8 consecutive logits from `base` (-inf past the end); one 32-byte load
+  // when the row is 16-byte aligned and the chunk is whole
+  const bool vec = (reinterpret_cast<uintptr_t>(lg) & 15) == 0;
+  auto load8 = [&](int base, float (&v)[kPerLane]) {
+    if (vec && base + kPerLane <= vocab) {
+      const float4 a = *reinterpret_cast<const float4*>(lg + base);
+      const float4 b = *reinterpret_cast<const float4*>(lg + base + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+      v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < kPerLane; ++e) v[e] = base + e < vocab ? lg[base + e] : -INFINITY;
+    }
+  };
+
+  // pass 1: maximum (and its first index, for greedy decoding); the next
+  // chunk is loaded before the current one is compared
   float mv = -INFINITY;
   int mi = 0x7FFFFFFF;
-  for (int i = tid; i < vocab; i += kSampleThreads) {
-    const float v = lg[i];
-    if (v > mv) { mv = v; mi = i; }
+  {
+    constexpr int STRIDE = kPerLane * kSampleThreads;
+    float cur[kPerLane], nxt[kPerLane];
+    int base = kPerLane * tid;
+    load8(base, cur);
+    for (; base < vocab; base += STRIDE) {
+      load8(base + STRIDE, nxt);
+#pragma unroll
+      for (int e = 0; e < kPerLane; ++e)
+        if (cur[e] > mv) { mv = cur[e]; mi = base + e; }
+#pragma unroll
+      for (int e = 0; e < kPerLane; ++e) cur[e] = nxt[e];
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -112,28 +146,28 @@ sample_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab,
   if (greedy) {
     token = am < vocab ? am : 0;
   } else {
-    // pass 2: segment sums, one 64-element segment per wave step
-    const int nseg = (vocab + 63) / 64;
-    for (int seg = wave; seg < nseg; seg += NW) {
-      const int i = seg * 64 + lane;
-      uint64_t w = i < vocab ? weight_of(lg[i], m, inv_t) : 0;
+    // pass 2: segment sums
+    const int nseg = (vocab + kSegment - 1) / kSegment;
+    {
+      float cur[kPerLane], nxt[kPerLane];
+      load8(wave * kSegment + kPerLane * lane, cur);
+      for (int seg = wave; seg < nseg; seg += NW) {
+        const int base = seg * kSegment + kPerLane * lane;
+        load8(base + NW * kSegment, nxt);
+        uint64_t w = 0;
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) w += shfl_xor_u64(w, o);
-      if (lane == 0) segsum[seg] = w;
+        for (int e = 0; e < kPerLane; ++e) w += weight_of(cur[e], m, inv_t);  // -inf weighs 0
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) w += shfl_xor_u64(w, o);
+        if (lane == 0) segsum[seg] = w;
+#pragma unroll
+        for (int e = 0; e < kPerLane; ++e) cur[e] = nxt[e];
+      }
     }
     __syncthreads();
-    // exclusive scan of the segment sums: thread t owns a contiguous run
-    constexpr int PER = kMaxSegments / kSampleThreads;
-    uint64_t loc[PER];
-    uint64_t run = 0;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int seg = tid * PER + k;
-      loc[k] = seg < nseg ? segsum[seg] : 0;
-      run += loc[k];
-    }
-    // inclusive scan of `run` over the block
-    uint64_t inc = run;
+    // exclusive scan of the segment sums: thread t owns segment t
+    const uint64_t mine = tid < nseg ? segsum[tid] : 0;
+    uint64_t inc = mine;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const uint64_t v = shfl_up_u64(inc, o);
@@ -151,30 +185,42 @@ sample_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab,
     } else {
       const uint64_t x = philox4x32_10(make_uint4((uint32_t)step, (uint32_t)cand[r], 0u, 0u), key).x;
       const uint64_t t = x * (total >> 32) + ((x * (total & 0xFFFFFFFFull)) >> 32);
-      uint64_t excl = wave_off + inc - run;
-#pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int seg = tid * PER + k;
-        if (seg < nseg && loc[k] > 0 && excl <= t && t < excl + loc[k]) {
-          found_seg = seg;
-          found_base = excl;
-        }
-        excl += loc[k];
+      const uint64_t excl = wave_off + inc - mine;
+      if (tid < nseg && mine > 0 && excl <= t && t < excl + mine) {
+        found_seg = tid;
+        found_base = excl;
       }
       __syncthreads();
-      // search inside the segment (wave 0)
+      // search inside the segment (wave 0): the lane, then the entry
       if (wave == 0) {
         const int seg = found_seg;
-        const int i = seg * 64 + lane;
-        uint64_t w = i < vocab ? weight_of(lg[i], m, inv_t) : 0;
-        uint64_t c = w;
+        const int base = seg * kSegment + kPerLane * lane;
+        float v[kPerLane];
+        load8(base, v);
+        uint64_t w[kPerLane];
+        uint64_t sum = 0;
+#pragma unroll
+        for (int e = 0; e < kPerLane; ++e) {
+          w[e] = weight_of(v[e], m, inv_t);  // -inf past the end weighs 0
+          sum += w[e];
+        }
+        uint64_t c = sum;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
           const uint64_t v = shfl_up_u64(c, o);
           if (lane >= o) c += v;
         }
         const uint64_t ballot = __ballot(found_base + c > t);
-        if (lane == 0) red_i[0] = seg * 64 + (int)__builtin_ctzll(ballot);
+        const int hit = (int)__builtin_ctzll(ballot);
+        if (lane == hit) {
+          uint64_t run = found_base + c - sum;
+          int e = 0;
+          for (; e < kPerLane - 1; ++e) {
+            run += w[e];
+            if (run > t) break;
+          }
+          red_i[0] = base + e;
+        }
       }
       __syncthreads();
       token = red_i[0];
@@ -190,7 +236,8 @@ sample_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab,
 
 void sample(const SampleArgs& a, hipStream_t s) {
   if (a.rows <= 0) return;
-  SR_REQUIRE(a.vocab >= 1 && (a.vocab + 63) / 64 <= kMaxSegments, 3, "vocabulary too large for the sampler");
+  SR_REQUIRE(a.vocab >= 1 && (a.vocab + kSegment - 1) / kSegment <= kMaxSegments, 3,
+             "vocabulary too large for the sampler");
   const int greedy = a.temperature == 0.0f;
   const float inv_t = greedy ? 1.0f : (float)(1.0 / (double)a.temperature);
   const uint2 key = make_uint2((uint32_t)a.seed, (uint32_t)(a.seed >> 32));

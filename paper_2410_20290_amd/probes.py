@@ -6,6 +6,8 @@
         21 rows, three launches each; prints the algorithmic bytes of each.
     python3 <repo>/paper_2410_20290_amd/probes.py gemm [rows,rows,...]
         Graph-replay timing of the projections at the given row counts.
+    python3 <repo>/paper_2410_20290_amd/probes.py sample
+        Timing of the sampler over 512, 103 and 21 rows of 8B-shaped logits.
     python3 <repo>/paper_2410_20290_amd/probes.py attn
         Timing of decode attention at the row counts and tail lengths of the
         three rounds of the 8B-shaped run.
@@ -135,9 +137,43 @@ def attn(cases):
         print(json.dumps({"rows": rows, "lt": lt, "us": round(t * 1e6, 1), "GBs": round(by / t / 1e9)}), flush=True)
 
 
+def sample_timing(rows_list):
+    """Graph-replay timing of the sampler over 8B-shaped logits rows."""
+    import torch
+    import paper_2410_20290_amd as sr
+    V = 128256
+    for rows in rows_list:
+        logits = torch.randn(rows, V, device="cuda") * 2.0
+        cand = torch.arange(rows, dtype=torch.int32, device="cuda")
+        tok = torch.empty(rows, dtype=torch.int32, device="cuda")
+        f = lambda: sr.sample(logits, cand, 7, 1.0, 42, tok)
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            f()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(10):
+                f()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 10 * 1e-3
+        print(json.dumps({"rows": rows, "vocab": V, "us": round(t * 1e6, 1),
+                          "GBs": round(rows * V * 4 / t / 1e9)}), flush=True)
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "traffic":
         traffic()
+    elif sys.argv[1] == "sample":
+        sample_timing([512, 103, 21])
     elif sys.argv[1] == "attn":
         attn([(512, 64), (512, 128), (103, 200), (103, 400), (103, 630), (21, 650), (21, 850), (21, 1020)])
     else:
