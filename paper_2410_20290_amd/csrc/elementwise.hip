@@ -1,5 +1,7 @@
 // Embedding gather, RMSNorm, RoPE (table + fused scatter into the KV cache),
 // the reward model's scalar head and small helpers.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 #include "philox.h"
@@ -165,120 +167,97 @@ void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, c
   SR_CHECK_LAUNCH();
 }
 
-// One block per row: h += sum of split partials (in split order); xn = RMSNorm(h) * g.
-// Threads own float4 column chunks; the chunks of one thread (up to 4 per
-// pass) are independent, so their loads are in flight together.
-template <typename T>
-__global__ void __launch_bounds__(256)
+// One block per row: h += sum of split partials (in split order); xn =
+// RMSNorm(h) * g.  Up to 1024 threads, each owning KV float4 chunks of the
+// row; the row and all its partials are loaded at once (the partial loads
+// of up to 8 splits are issued together and added in split order), the new
+// h stays in registers for the normalisation.
+template <typename T, int KV>
+__global__ void __launch_bounds__(1024)
 add_norm_kernel(const float* __restrict__ part, int splits, int rows, int d, float* __restrict__ h,
                 const T* __restrict__ g, float eps, T* __restrict__ xn) {
-  __shared__ float red[4];
-  const int r = blockIdx.x;
+  __shared__ float red[16];
+  const int r = blockIdx.x, nt = blockDim.x, tid = threadIdx.x;
   const int d4 = d / 4;
   float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
   const float4* pr = reinterpret_cast<const float4*>(part + (int64_t)r * d);
   const int64_t sstride4 = (int64_t)rows * d4;
-  float ss = 0.f;
-  for (int base = 0; base < d4; base += 4 * 256) {
-    float4 v[4];
-    bool ok[4];
+  float4 v[KV];
+  bool ok[KV];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int j = base + u * 256 + threadIdx.x;
-      ok[u] = j < d4;
-      v[u] = ok[u] ? hr[j] : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    for (int sp = 0; sp < splits; ++sp) {
+  for (int k = 0; k < KV; ++k) {
+    const int j = tid + k * nt;
+    ok[k] = j < d4;
+    v[k] = hr[ok[k] ? j : 0];
+  }
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float4 p[8][KV];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = base + u * 256 + threadIdx.x;
-        if (ok[u]) {
-          const float4 p = pr[sp * sstride4 + j];
-          v[u].x += p.x; v[u].y += p.y; v[u].z += p.z; v[u].w += p.w;
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int k = 0; k < KV; ++k) {
+        const int j = ok[k] ? tid + k * nt : 0;
+        p[u][k] = s0 + u < splits ? pr[(s0 + u) * sstride4 + j] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int k = 0; k < KV; ++k)
+        if (s0 + u < splits) {
+          v[k].x += p[u][k].x; v[k].y += p[u][k].y; v[k].z += p[u][k].z; v[k].w += p[u][k].w;
         }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int j = base + u * 256 + threadIdx.x;
-      if (ok[u]) {
-        hr[j] = v[u];
-        ss += v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
-      }
-    }
   }
-  ss = block_sum256(ss, red);
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  const float* hs = h + (int64_t)r * d;
-  T* o = xn + (int64_t)r * d;
-  for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f32<T>(hs[i] * inv * to_f32<T>(g[i]));
-}
-
-// Row-parallel form for few rows: grid (rows, ceil(d / 1024)).  The first
-// kernel adds the split partials into h and leaves each block's sum of
-// squares; the second sums those in block order and normalises.
-__global__ void __launch_bounds__(256)
-add_rows_kernel(const float* __restrict__ part, int splits, int rows, int d, float* __restrict__ h,
-                float* __restrict__ ssp) {
-  __shared__ float red[4];
-  const int r = blockIdx.x, blk = blockIdx.y, nblk = gridDim.y;
-  const int d4 = d / 4;
-  const int j = blk * 256 + threadIdx.x;
   float ss = 0.f;
-  if (j < d4) {
-    float4* hr = reinterpret_cast<float4*>(h + (int64_t)r * d);
-    const float4* pr = reinterpret_cast<const float4*>(part + (int64_t)r * d);
-    const int64_t sstride4 = (int64_t)rows * d4;
-    float4 v = hr[j];
-    for (int sp = 0; sp < splits; ++sp) {
-      const float4 p = pr[sp * sstride4 + j];
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
-    }
-    hr[j] = v;
-    ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+  for (int k = 0; k < KV; ++k)
+    if (ok[k]) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+  // block sum in a fixed order: waves, then the wave totals in wave order
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int w = 0; w < (nt >> 6); ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  T* o = xn + (int64_t)r * d;
+#pragma unroll
+  for (int k = 0; k < KV; ++k) {
+    if (!ok[k]) continue;
+    const int j = tid + k * nt;
+    hr[j] = v[k];
+    const int c = 4 * j;
+    o[c] = from_f32<T>(v[k].x * inv * to_f32<T>(g[c]));
+    o[c + 1] = from_f32<T>(v[k].y * inv * to_f32<T>(g[c + 1]));
+    o[c + 2] = from_f32<T>(v[k].z * inv * to_f32<T>(g[c + 2]));
+    o[c + 3] = from_f32<T>(v[k].w * inv * to_f32<T>(g[c + 3]));
   }
-  ss = block_sum256(ss, red);
-  if (threadIdx.x == 0) ssp[(int64_t)r * nblk + blk] = ss;
 }
 
 template <typename T>
-__global__ void __launch_bounds__(256)
-norm_rows_kernel(const float* __restrict__ h, int d, const float* __restrict__ ssp, const T* __restrict__ g,
-                 float eps, T* __restrict__ xn) {
-  const int r = blockIdx.x, blk = blockIdx.y, nblk = gridDim.y;
-  float ss = 0.f;
-  for (int b = 0; b < nblk; ++b) ss += ssp[(int64_t)r * nblk + b];
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  const int c0 = blk * 1024, c1 = min(d, c0 + 1024);
-  const float* hr = h + (int64_t)r * d;
-  T* o = xn + (int64_t)r * d;
-  for (int i = c0 + threadIdx.x; i < c1; i += 256) o[i] = from_f32<T>(hr[i] * inv * to_f32<T>(g[i]));
+static void launch_add_norm(const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
+                            void* xn, hipStream_t s) {
+  const int d4 = d / 4;
+  const int nt = std::min(1024, (d4 + 63) / 64 * 64);
+  const int kv = (d4 + nt - 1) / nt;
+  SR_REQUIRE(kv <= 4, 3, "d_model too large for add_norm");
+  if (kv == 1)
+    hipLaunchKernelGGL((add_norm_kernel<T, 1>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+                       (const T*)g, eps, (T*)xn);
+  else if (kv == 2)
+    hipLaunchKernelGGL((add_norm_kernel<T, 2>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+                       (const T*)g, eps, (T*)xn);
+  else
+    hipLaunchKernelGGL((add_norm_kernel<T, 4>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+                       (const T*)g, eps, (T*)xn);
+  SR_CHECK_LAUNCH();
 }
 
 void add_norm(int dtype, const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
-              void* xn, float* ssp, hipStream_t s) {
+              void* xn, hipStream_t s) {
   if (rows <= 0) return;
   SR_REQUIRE(d % 4 == 0, 3, "d_model must be a multiple of 4");
-  if (ssp && rows < 256) {
-    dim3 grid(rows, (d + 1023) / 1024);
-    hipLaunchKernelGGL(add_rows_kernel, grid, dim3(256), 0, s, part, splits, rows, d, h, ssp);
-    SR_CHECK_LAUNCH();
-    if (dtype == SR_BF16)
-      hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, grid, dim3(256), 0, s, h, d, ssp, (const bf16_t*)g, eps,
-                         (bf16_t*)xn);
-    else
-      hipLaunchKernelGGL(norm_rows_kernel<float>, grid, dim3(256), 0, s, h, d, ssp, (const float*)g, eps,
-                         (float*)xn);
-    SR_CHECK_LAUNCH();
-    return;
-  }
-  if (dtype == SR_BF16)
-    hipLaunchKernelGGL(add_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, part, splits, rows, d, h,
-                       (const bf16_t*)g, eps, (bf16_t*)xn);
-  else
-    hipLaunchKernelGGL(add_norm_kernel<float>, dim3(rows), dim3(256), 0, s, part, splits, rows, d, h,
-                       (const float*)g, eps, (float*)xn);
-  SR_CHECK_LAUNCH();
+  if (dtype == SR_BF16) launch_add_norm<bf16_t>(part, splits, rows, d, h, g, eps, xn, s);
+  else launch_add_norm<float>(part, splits, rows, d, h, g, eps, xn, s);
 }
 
 // Grid (rows, hq + 2 hkv), one wave per (row, head): sum the split partials

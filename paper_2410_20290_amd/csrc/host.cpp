@@ -204,7 +204,6 @@ struct Layout {
   int32_t* ctok; int32_t* clen; float* ch; void* cxn; float* cqkv; float* cq; void* ck; void* cv;
   void* co; void* cu;
   float* gpart;
-  float* ssp;  // per-block sums of squares of the row-parallel RMSNorm
 };
 
 static Layout carve(void* base, const Dims& g, const Dims& rm, const Plan& pl, size_t* total) {
@@ -253,7 +252,6 @@ static Layout carve(void* base, const Dims& g, const Dims& rm, const Plan& pl, s
   L.co = a.bytes((size_t)Tc * chq * g.es);
   L.cu = a.bytes((size_t)Tc * cff * g.es);
   L.gpart = a.take<float>(pl.gpart);
-  L.ssp = a.take<float>((size_t)N * ((g.d + 1023) / 1024));
   *total = a.off + 256;
   return L;
 }
@@ -472,14 +470,14 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
     sp = run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_PARTIAL,
                   nullptr, 0, 0);
     run_other(c, (double)rows * m.d * (4.0 * sp + 8 + m.es), [&] {
-      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, G.ffn_norm(l), m.eps, L.xn, L.ssp, c.s);
+      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, G.ffn_norm(l), m.eps, L.xn, c.s);
     });
     run_gemm(c, true, m.dtype, L.xn, m.d, G.w13(l), m.d, rows, m.ff, m.d, EPI_STORE, L.u, m.ff, bf, true,
              (int64_t)m.ff * m.d);
     sp = run_gemm(c, true, m.dtype, L.u, m.ff, G.w2(l), m.ff, rows, m.d, m.ff, EPI_PARTIAL, nullptr, 0, 0);
     const void* gnext = l + 1 < m.nl ? G.attn_norm(l + 1) : G.w->final_norm;
     run_other(c, (double)rows * m.d * (4.0 * sp + 8 + m.es), [&] {
-      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, gnext, m.eps, L.xn, L.ssp, c.s);
+      add_norm(m.dtype, L.gpart, sp, rows, m.d, L.h, gnext, m.eps, L.xn, c.s);
     });
   }
   run_gemm(c, true, m.dtype, L.xn, m.d, G.w->head, m.d, rows, m.V, m.d, EPI_STORE, L.logits, m.V, 0);

@@ -65,9 +65,8 @@ void philox_fill(uint64_t seed, const uint32_t* ctr, int n, uint32_t* out, hipSt
 void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, const void* g, float eps,
                 float* h, void* xn, hipStream_t s);
 // h[r] += sum_s part[s][r]; xn[r] = RMSNorm(h[r]) * g (model dtype); d columns.
-// ssp (rows * ceil(d/1024) floats, may be null) enables the row-parallel form.
 void add_norm(int dtype, const float* part, int splits, int rows, int d, float* h, const void* g, float eps,
-              void* xn, float* ssp, hipStream_t s);
+              void* xn, hipStream_t s);
 // qkv[r] = sum_s part[s][r] (rows of (hq + 2 hkv) hd); RoPE at position pos
 // on q and k; q -> qout[r][hq][hd] (fp32); k, v -> kdst/vdst[r][hkv][cap][hd]
 // at token t0.
