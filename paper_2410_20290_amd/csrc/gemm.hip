@@ -568,16 +568,24 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // For the decode projections (a few hundred rows at most) the weights are
 // streamed once from HBM; what matters is keeping enough of them in flight
 // and keeping the per-step overhead small.  Block tile BM x BN (PAIRED: BN
-// gate rows then BN up rows, BN output columns), K step 128, NST LDS stages
-// filled by global_load_lds_dwordx4 up to NST - 1 steps ahead, one barrier
-// per step.  LDS stage: the BM activation rows then the weight rows, 256
-// bytes each, 16-byte chunk c of row r in slot c ^ (r & 15) (conflict-free
-// fragment reads).  4 waves in a WGM x WGN grid, each a (BM / WGM) x
-// (BN / WGN) tile of v_mfma_f32_16x16x32_bf16 accumulators; the fragment
-// reads of the next 32-wide sub-step run under the MFMAs of the current one.
+// gate rows then BN up rows, BN output columns), K step BK (64 or 128), NST
+// LDS stages filled by global_load_lds_dwordx4 up to NST - 1 steps ahead,
+// one barrier per step.  LDS stage: the BM activation rows then the weight
+// rows, 2 BK bytes each; 16-byte chunk c of row r sits in slot c ^ (r & 15)
+// (BK 128) or c ^ (r & 7) ^ ((r >> 3) & 1) (BK 64), so the fragment reads of
+// 16 consecutive rows are free of bank conflicts.  4 waves in a WGM x WGN
+// grid, each a (BM / WGM) x (BN / WGN) tile of v_mfma_f32_16x16x32_bf16
+// accumulators; the fragment reads of the next 32-wide sub-step run under
+// the MFMAs of the current one.
 #define SR_VMB(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
-template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED>
+template <int BK>
+__device__ __forceinline__ int stream_slot(int c, int r) {
+  if constexpr (BK == 128) return c ^ (r & 15);
+  else return c ^ (r & 7) ^ ((r >> 3) & 1);
+}
+
+template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED, int BK>
 __global__ void __launch_bounds__(256)
 gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
                    int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
@@ -585,10 +593,14 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   constexpr int NB = PAIRED ? 2 : 1;
   constexpr int BNL = NB * BN;                  // weight rows per tile
   constexpr int ROWS = BM + BNL;
-  constexpr int BK = 128, STAGE = ROWS * BK;    // bf16 elements per stage
-  constexpr int D = ROWS / 16;                  // DMA instructions per wave per stage
+  constexpr int STAGE = ROWS * BK;              // bf16 elements per stage
+  constexpr int CH = BK / 8;                    // 16-byte chunks per row
+  constexpr int RPI = 64 / CH;                  // rows per DMA instruction (1 KB)
+  constexpr int D = ROWS / (4 * RPI);           // DMA instructions per wave per stage
+  constexpr int NS = BK / 32;                   // MFMA sub-steps per stage
   constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
-  static_assert(ROWS % 16 == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1, "tile shape");
+  static_assert((BK == 64 || BK == 128) && ROWS % (4 * RPI) == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1,
+                "tile shape");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
 
   const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, K / k_per_split);
@@ -600,15 +612,15 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   const int k_begin = tile.split * k_per_split;
   const int nk = k_per_split / BK;
 
-  // DMA instruction j covers tile rows 4 j .. 4 j + 3 (activation rows
-  // first); wave w issues j = w + 4 q.  Lane l writes slot l % 16 of row
-  // l / 16 and fetches the chunk stored there; rows past M or N are clamped
-  // (their results are never stored).
+  // DMA instruction j covers tile rows RPI j .. RPI j + RPI - 1 (activation
+  // rows first); wave w issues j = w + 4 q.  Lane l writes slot l % CH of
+  // row l / CH and fetches the chunk stored there; rows past M or N are
+  // clamped (their results are never stored).
   uint32_t off[D];
 #pragma unroll
   for (int q = 0; q < D; ++q) {
-    const int r = 4 * (wave + 4 * q) + (lane >> 4);
-    const int c = (lane & 15) ^ (r & 15);
+    const int r = RPI * (wave + 4 * q) + lane / CH;
+    const int c = stream_slot<BK>(lane % CH, r);
     int64_t e;
     if (r < BM) {
       e = (int64_t)min(m0 + r, M - 1) * lda;
@@ -625,17 +637,17 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     const int kb = st * BK * 2;
 #pragma unroll
     for (int q = 0; q < D; ++q) {
-      const bool is_a = 4 * (wave + 4 * q) < BM;  // wave-uniform
+      const bool is_a = RPI * (wave + 4 * q) < BM;  // wave-uniform
       dma16((is_a ? Ab : Bb) + kb + off[q], dst + (wave + 4 * q) * 512);
     }
   };
 
   // 16x16x32 fragments: lane l holds row l % 16 of a 16-row block, K chunk
-  // 4 s + l / 16 of sub-step s (s < 4), stored in slot chunk ^ (l % 16).
+  // 4 s + l / 16 of sub-step s.
   const int fr = lane & 15, fg = lane >> 4;
-  int foff[4];
+  int foff[NS];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) foff[s] = fr * BK + 8 * ((4 * s + fg) ^ fr);
+  for (int s = 0; s < NS; ++s) foff[s] = fr * BK + 8 * stream_slot<BK>(4 * s + fg, fr);
 
   f32x4 acc[NB][TI][TJ];
 #pragma unroll
@@ -662,7 +674,6 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
         for (int j = 0; j < TJ; ++j)
           acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
   };
-
   // one MFMA, then one fragment read of the next sub-step, alternating;
   // then the remaining MFMAs
   constexpr int NMF = NB * TI * TJ, NRD = TI + NB * TJ;
@@ -696,12 +707,14 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     read_frags(base, 1, a1, b1);
     mfma(a0, b0);
     interleave();
-    read_frags(base, 2, a0, b0);
-    mfma(a1, b1);
-    interleave();
-    read_frags(base, 3, a1, b1);
-    mfma(a0, b0);
-    interleave();
+    if constexpr (NS == 4) {
+      read_frags(base, 2, a0, b0);
+      mfma(a1, b1);
+      interleave();
+      read_frags(base, 3, a1, b1);
+      mfma(a0, b0);
+      interleave();
+    }
     mfma(a1, b1);
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -1005,6 +1018,17 @@ static int stream_max_rows() {
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
 
+// Rows below which the 128 x 128 streaming tile (K step 64) takes over from
+// the other tiles for unpaired projections with at most 65536 outputs per
+// row; off by default (it measured even with them end to end).
+static int stream_mid_max_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_STREAM_MID_MAX_M");
+    return e ? atoi(e) : 0;
+  }();
+  return v;
+}
+
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
@@ -1013,6 +1037,7 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.dma = false;
   p.stream = 0;
   p.stream_bn = 0;
+  p.stream_bk = 128;
   if (dtype != SR_BF16) return p;
   if (M <= stream_max_rows() && K % 128 == 0 && (M <= 64 || N <= 65536)) {
     // One round of work-groups (one per CU): split K by the largest power of
@@ -1022,6 +1047,19 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     const int64_t tiles = (int64_t)((M + p.stream - 1) / p.stream) * ((N + p.stream_bn - 1) / p.stream_bn);
     int splits = 1;
     while (tiles * splits * 2 <= 256 && K % (splits * 2 * 128) == 0) splits *= 2;
+    p.splits = splits;
+    return p;
+  }
+  if (M > stream_max_rows() && M < stream_mid_max_rows() && K % 64 == 0 && N <= 65536 && !paired) {
+    // A few hundred rows (the first decode round): 128 x 128 tiles with a K
+    // step of 64, split K as above (the paired gate|up projection keeps the
+    // 256 x 256 tile).
+    p.stream = 128;
+    p.stream_bn = paired ? 64 : 128;
+    p.stream_bk = 64;
+    const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + p.stream_bn - 1) / p.stream_bn);
+    int splits = 1;
+    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 64) == 0 && K / (splits * 2) >= 512) splits *= 2;
     p.splits = splits;
     return p;
   }
@@ -1146,10 +1184,19 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   } else if (plan.stream && dma_offsets_fit(g)) {
     dim3 grid = tile_grid((g.M + plan.stream - 1) / plan.stream, (g.N + plan.stream_bn - 1) / plan.stream_bn, splits);
 #define SR_STREAM(BM, BN, WGM, WGN, NST, P)                                                              \
-  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P>), grid, dim3(256), 0, s,               \
+  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, 128>), grid, dim3(256), 0, s,          \
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, \
                      part)
-    if (plan.stream == 32) {
+    if (plan.stream_bk == 64) {
+      if (g.paired)
+        hipLaunchKernelGGL((gemm_stream_kernel<128, 64, 2, 2, 4, true, 64>), grid, dim3(256), 0, s,
+                           (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e,
+                           part);
+      else
+        hipLaunchKernelGGL((gemm_stream_kernel<128, 128, 2, 2, 4, false, 64>), grid, dim3(256), 0, s,
+                           (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e,
+                           part);
+    } else if (plan.stream == 32) {
       if (g.paired) SR_STREAM(32, 64, 1, 4, 3, true);
       else SR_STREAM(32, 64, 1, 4, 5, false);
     } else if (plan.stream == 64) {

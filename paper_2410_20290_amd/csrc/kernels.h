@@ -34,6 +34,7 @@ struct GemmPlan {
   bool dma;     // 256 x 256 tile fed by LDS DMA
   int stream;     // > 0: LDS-DMA streaming kernel for few rows, tile height
   int stream_bn;  // its tile width (output columns)
+  int stream_bk;  // its K step
 };
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired);
 size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired);
