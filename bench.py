@@ -105,6 +105,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)
     ap.add_argument("--cpu-steps", type=int, default=48)
+    ap.add_argument("--reward", choices=["model", "logprob"], default="model",
+                    help="partial reward: the reward model, or the generator's mean log-probability "
+                         "(section 5.3, no reward model)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the hot path is one GPU's batch of "
@@ -129,21 +132,22 @@ def main():
     rw = synth.model_weights(m, cfg.rm_seed, True)
     prompt = synth.prompt(cfg)
     log(f"[bench] weights generated in {time.time() - t:.1f}s")
+    kind = sr.SR_REWARD_LOGPROB if args.reward == "logprob" else sr.SR_REWARD_MODEL
     gen = sr.DeviceModel.upload(m, gw, False)
-    rm = sr.DeviceModel.upload(m, rw, True)
+    rm = sr.DeviceModel.upload(m, rw, True) if kind == sr.SR_REWARD_MODEL else None
     del rw
     torch.cuda.synchronize()
     log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
 
     p = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                       cfg.eos_id, 0, 0)
+                       cfg.eos_id, 0, 0, kind)
     ws = sr.Workspace(gen, rm, len(prompt), p)
     log(f"[bench] workspace {ws.nbytes / 2**30:.2f} GiB")
     for i in range(args.warmup):
         o = sr.generate(gen, rm, prompt, p, ws)
         log(f"[bench] warmup {i}: {o['sec_total']:.3f}s generated={o['generated_tokens']}")
     pp = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                        cfg.eos_id, 0, args.profile_every)
+                        cfg.eos_id, 0, args.profile_every, kind)
     kern = {}
     gen_tokens = 0
     results = []
@@ -169,7 +173,7 @@ def main():
     bon = None
     if not args.no_bon and cfg.alpha > 0:
         pb = sr.make_params(cfg.n, 0.0, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                            cfg.eos_id, 0, 0)
+                            cfg.eos_id, 0, 0, kind)
         wsb = sr.Workspace(gen, rm, len(prompt), pb)
         torch.cuda.synchronize()
         tb = time.perf_counter()
@@ -215,8 +219,12 @@ def main():
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(s_per_prompt * 1e3, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": m.dtype, "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: 8B-shaped bf16 generator + reward model, prompt {cfg.prompt_len}, "
+        "config": {"workload": f"{cfg.name}: 8B-shaped bf16 generator + "
+                               + ("reward model" if kind == sr.SR_REWARD_MODEL else
+                                  "mean log-probability reward (no reward model)")
+                               + f", prompt {cfg.prompt_len}, "
                                f"N={cfg.n}, tau={cfg.tau}, alpha={cfg.alpha}, {cfg.max_new_tokens} new tokens",
+                   "reward": args.reward,
                    "N": cfg.n, "alpha": cfg.alpha, "tau": cfg.tau, "max_new_tokens": cfg.max_new_tokens,
                    "prompt_len": cfg.prompt_len},
         "s_per_prompt": round(s_per_prompt, 4),

@@ -104,7 +104,13 @@ typedef struct {
  *  profile_every  0 = off; k > 0 = time kernels with HIP events on `stream`
  *               during every k-th decode step and every reward/cut phase,
  *               accumulating into sr_result.kernel_* (costs one host
- *               synchronisation per timed step). */
+ *               synchronisation per timed step).
+ *  reward_kind  SR_REWARD_MODEL: s(x, y) is the reward model `rm`;
+ *               SR_REWARD_LOGPROB: s(y) = (1/len(y)) ln p(y | x) under the
+ *               generator's own softmax at temperature 1 (section 5.3),
+ *               accumulated during sampling; `rm` is not evaluated and may
+ *               be NULL. */
+enum { SR_REWARD_MODEL = 0, SR_REWARD_LOGPROB = 1 };
 typedef struct {
   int32_t n;
   double alpha;
@@ -114,6 +120,7 @@ typedef struct {
   int32_t eos_id;
   int32_t max_rounds;
   int32_t profile_every;
+  int32_t reward_kind;
 } sr_params;
 
 /* Kernel classes of sr_result.kernel_*. */

@@ -70,6 +70,21 @@ def arg_best(scores: dict) -> int:
     return top_k(list(scores), scores, 1)[0]
 
 
+def mean_logprob(gen, prompt, tokens) -> float:
+    """The probability-as-reward score of section 5.3:
+    s(y) = (1 / len(y)) ln p(y | x), with p the generator's own softmax
+    (temperature 1) and ln p(y | x) the sum over the response tokens of
+    ln p(y_t | x, y_<t).  Computed in float64 from one forward pass over
+    x + y: row P - 1 + t of the logits gives the distribution of y_t."""
+    P, n = len(prompt), len(tokens)
+    if n == 0:
+        return 0.0
+    lg = gen.logits(list(prompt) + list(tokens))[P - 1:P - 1 + n]
+    m = lg.max(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(np.exp(lg - m).sum(axis=1))
+    return float(np.mean(lg[np.arange(n), list(tokens)] - lse))
+
+
 def _f32(x) -> float:
     return float(np.float32(x))
 

@@ -48,7 +48,7 @@ KERNEL_CLASSES = ["gen_gemm_mfma", "gen_gemm_hbm", "decode_attn", "rm_gemm", "pr
 class sr_params(ctypes.Structure):
     _fields_ = [("n", _i32), ("alpha", _f64), ("tau", _i32), ("max_new_tokens", _i32),
                 ("temperature", _f32), ("seed", _u64), ("eos_id", _i32), ("max_rounds", _i32),
-                ("profile_every", _i32)]
+                ("profile_every", _i32), ("reward_kind", _i32)]
 
 
 class sr_result(ctypes.Structure):
@@ -112,6 +112,12 @@ def lib():
     return _lib
 
 
+def _mref(m):
+    """Pointer to a model descriptor, or NULL for None (a reward model is not
+    needed when the reward is the generator's own log-probability)."""
+    return None if m is None else ctypes.byref(m.desc)
+
+
 def last_error() -> str:
     return lib().sr_last_error().decode()
 
@@ -163,14 +169,18 @@ class DeviceModel:
         return DeviceModel(shape, reward, ts, sr_model(cfg, w))
 
 
+SR_REWARD_MODEL, SR_REWARD_LOGPROB = 0, 1
+
+
 def make_params(n, alpha, tau, max_new_tokens, temperature=1.0, seed=42, eos_id=-1, max_rounds=0,
-                profile_every=0) -> sr_params:
-    return sr_params(n, alpha, tau, max_new_tokens, temperature, seed, eos_id, max_rounds, profile_every)
+                profile_every=0, reward_kind=SR_REWARD_MODEL) -> sr_params:
+    return sr_params(n, alpha, tau, max_new_tokens, temperature, seed, eos_id, max_rounds, profile_every,
+                     reward_kind)
 
 
 def workspace_size(gen: DeviceModel, rm: DeviceModel, prompt_len: int, p: sr_params) -> int:
     out = ctypes.c_size_t(0)
-    _check(lib().sr_workspace_size(ctypes.byref(gen.desc), ctypes.byref(rm.desc), prompt_len, ctypes.byref(p),
+    _check(lib().sr_workspace_size(ctypes.byref(gen.desc), _mref(rm), prompt_len, ctypes.byref(p),
                                    ctypes.byref(out)))
     return int(out.value)
 
@@ -208,7 +218,7 @@ def generate(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, ws: Worksp
                       all_tokens=np.zeros((n, p.max_new_tokens), np.int32), all_len=np.zeros(n, np.int32),
                       final_scores=np.zeros(n, np.float32))
         tr = sr_trace(*[a.ctypes.data for a in arrays.values()], R)
-    st = lib().sr_generate(ctypes.byref(gen.desc), ctypes.byref(rm.desc), prompt.ctypes.data, len(prompt),
+    st = lib().sr_generate(ctypes.byref(gen.desc), _mref(rm), prompt.ctypes.data, len(prompt),
                            ctypes.byref(p), ws.ptr, ws.nbytes, _stream(stream), out_tokens.ctypes.data,
                            ctypes.byref(res), ctypes.byref(tr) if tr is not None else None)
     _check(st)
@@ -282,7 +292,7 @@ def logits_teacher_forced(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_param
     prompt = np.ascontiguousarray(np.asarray(prompt, dtype=np.int32))
     rows, length = tokens.shape
     out = torch.empty((rows, length, gen.shape.vocab), dtype=torch.float32, device=tokens.device)
-    _check(lib().sr_logits_teacher_forced(ctypes.byref(gen.desc), ctypes.byref(rm.desc), prompt.ctypes.data,
+    _check(lib().sr_logits_teacher_forced(ctypes.byref(gen.desc), _mref(rm), prompt.ctypes.data,
                                           len(prompt), ctypes.byref(p), _ptr(tokens), rows, length, _ptr(out),
                                           ws.ptr, ws.nbytes, _stream(stream)))
     return out
@@ -295,7 +305,7 @@ def reward_scores(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, token
     prompt = np.ascontiguousarray(np.asarray(prompt, dtype=np.int32))
     rows, max_len = tokens.shape
     out = torch.empty(rows, dtype=torch.float32, device=tokens.device)
-    _check(lib().sr_reward_scores(ctypes.byref(gen.desc), ctypes.byref(rm.desc), prompt.ctypes.data,
+    _check(lib().sr_reward_scores(ctypes.byref(gen.desc), _mref(rm), prompt.ctypes.data,
                                   len(prompt), ctypes.byref(p), _ptr(tokens), _ptr(lens), rows, max_len, _ptr(out),
                                   ws.ptr, ws.nbytes, _stream(stream)))
     return out

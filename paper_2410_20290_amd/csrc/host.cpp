@@ -94,6 +94,21 @@ static void check_params(const sr_params* p, const sr_model* gen) {
              "eos_id must be -1 or a token id");
   SR_REQUIRE(p->max_rounds >= 0, SR_ERR_INVALID_ARG, "max_rounds must be >= 0");
   SR_REQUIRE((int64_t)p->n * p->tau <= (int64_t)1 << 31, SR_ERR_INVALID_ARG, "n * tau too large");
+  SR_REQUIRE(p->reward_kind == SR_REWARD_MODEL || p->reward_kind == SR_REWARD_LOGPROB, SR_ERR_INVALID_ARG,
+             "reward_kind must be SR_REWARD_MODEL or SR_REWARD_LOGPROB");
+}
+
+// The reward model of a run: `rm`, or (log-probability reward without a
+// reward model) a stand-in of the generator's shape that only sizes the
+// workspace and is never evaluated.
+static const sr_model* reward_model_of(const sr_model* gen, const sr_model* rm, const sr_params* p,
+                                       sr_model* stand_in) {
+  if (rm != nullptr) return rm;
+  SR_REQUIRE(p != nullptr && p->reward_kind == SR_REWARD_LOGPROB && gen != nullptr, SR_ERR_INVALID_ARG,
+             "rm is NULL (allowed only with reward_kind = SR_REWARD_LOGPROB)");
+  *stand_in = *gen;
+  stand_in->cfg.is_reward = 1;
+  return stand_in;
 }
 
 // ------------------------------------------------------------ planning
@@ -199,6 +214,7 @@ struct Layout {
   State st[3];
   int32_t *i_cand, *i_len, *i_count, *best, *count, *count2;
   float *i_score, *score, *score2;
+  float* lp_sum;            // [N] running ln p of each candidate's response (indexed by candidate)
   int32_t *accept, *src_row, *src_row2, *src_tmp;
   float* h; void* xn; float* qkv; float* q; void* o; void* u; float* logits; float* apart;
   int32_t* ctok; int32_t* clen; float* ch; void* cxn; float* cqkv; float* cq; void* ck; void* cv;
@@ -227,6 +243,7 @@ static Layout carve(void* base, const Dims& g, const Dims& rm, const Plan& pl, s
   L.i_count = a.take<int32_t>(1); L.best = a.take<int32_t>(1);
   L.count = a.take<int32_t>(1); L.count2 = a.take<int32_t>(1);
   L.score = a.take<float>(N); L.score2 = a.take<float>(N);
+  L.lp_sum = a.take<float>(N);
   L.accept = a.take<int32_t>(N); L.src_row = a.take<int32_t>(N); L.src_row2 = a.take<int32_t>(N);
   L.src_tmp = a.take<int32_t>(N);
   L.h = a.take<float>((size_t)N * g.d);
@@ -494,13 +511,14 @@ static void prompt_logits(const Ctx& c, const Model& G) {
 }
 
 __global__ void init_state_kernel(int n, int32_t* cand, int32_t* len, int32_t* done, int32_t* cand_len,
-                                  int32_t* i_count) {
+                                  int32_t* i_count, float* lp_sum) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) {
     cand[i] = i;
     len[i] = 0;
     done[i] = 0;
     cand_len[i] = 0;
+    lp_sum[i] = 0.f;
   }
   if (i == 0) *i_count = 0;
 }
@@ -583,9 +601,19 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   prof.s = s;
   const int every = p->profile_every;
   Ctx c{&pl, &L, s, every > 0 ? &prof : nullptr};
-  Model G{gd, &gen->w}, R{rd, &rm->w};
+  const bool lp_mode = p->reward_kind == SR_REWARD_LOGPROB;
+  Model G{gd, &gen->w}, R{rd, lp_mode ? nullptr : &rm->w};
   const int N = pl.N, Lmax = pl.Lmax;
   std::memset(out, 0, sizeof(*out));
+  // partial rewards of the rows of a round: the reward model, or the mean
+  // log-probability accumulated while sampling (section 5.3)
+  auto score_rows = [&](const State& st, int b, int D) {
+    if (lp_mode) {
+      logprob_scores(L.lp_sum, st.cand, st.len, b, L.score, s);
+    } else {
+      reward_rows(c, R, st.cand, st.len, b, D, L.score);
+    }
+  };
   Timer tall(s), tph(s);
   tall.start();
 
@@ -593,13 +621,15 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   prof.active = every > 0;
   tph.start();
   rope_table(L.rope_g, P + Lmax + 1, gd.hd, gd.theta, s);
-  rope_table(L.rope_r, P + Lmax + 1, rd.hd, rd.theta, s);
   copy_h2d(L.ctok, prompt, sizeof(int32_t) * P, s);
-  prompt_prefill(c, R, L.rope_r, L.rpre);
+  if (!lp_mode) {
+    rope_table(L.rope_r, P + Lmax + 1, rd.hd, rd.theta, s);
+    prompt_prefill(c, R, L.rope_r, L.rpre);
+  }
   prompt_prefill(c, G, L.rope_g, L.gpre);
   prompt_logits(c, G);
   hipLaunchKernelGGL(init_state_kernel, dim3((N + 255) / 256), dim3(256), 0, s, N, L.st[0].cand,
-                     L.st[0].len, L.st[0].done, L.cand_len, L.i_count);
+                     L.st[0].len, L.st[0].done, L.cand_len, L.i_count, L.lp_sum);
   SR_CHECK_LAUNCH();
   out->sec_prefill = tph.stop();
   prof.flush();
@@ -625,6 +655,10 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
       sa.next_tok = st.tok; sa.done = st.done; sa.len = st.len; sa.store = L.store;
       sa.store_ld = Lmax; sa.eos_id = p->eos_id;
       timed(c, SR_K_SAMPLE, (double)b * gd.V * 4, 0.0, [&] { sample(sa, s); });
+      if (lp_mode)
+        timed(c, SR_K_SAMPLE, (double)b * gd.V * 4, 0.0, [&] {
+          logprob_accumulate(L.logits, sa.row_stride, b, gd.V, st.cand, st.tok, st.len, step, L.lp_sum, s);
+        });
       if (prof.active) prof.flush();
     }
     prof.active = every > 0;
@@ -641,7 +675,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     if (D == Lmax || unfinished == 0) {
       // every candidate of this round is complete: score all, all join I
       tph.start();
-      reward_rows(c, R, st.cand, st.len, b, D, L.score);
+      score_rows(st, b, D);
       out->sec_reward += tph.stop();
       CutArgs ca;
       std::memset(&ca, 0, sizeof(ca));
@@ -660,7 +694,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     const int K = keep_of(b, pl.appm);
     SR_REQUIRE(K < b, SR_ERR_INTERNAL, "decision point without a possible rejection");
     tph.start();
-    reward_rows(c, R, st.cand, st.len, b, D, L.score);
+    score_rows(st, b, D);
     out->sec_reward += tph.stop();
     tph.start();
     const int nxt = 1 - cur;
@@ -877,7 +911,7 @@ static void reward_entry(const sr_model* gen, const sr_model* rm, const int32_t*
   SR_HIP(hipMemcpy2DAsync(L.store, (size_t)pl.Lmax * 4, tokens, (size_t)max_len * 4, (size_t)max_len * 4,
                           rows, hipMemcpyDeviceToDevice, s));
   hipLaunchKernelGGL(init_state_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, rows, L.st[0].cand,
-                     L.st[0].len, L.st[0].done, L.cand_len, L.i_count);
+                     L.st[0].len, L.st[0].done, L.cand_len, L.i_count, L.lp_sum);
   SR_CHECK_LAUNCH();
   reward_rows(c, R, L.st[0].cand, lens, rows, max_len, scores);
   SR_HIP(hipStreamSynchronize(s));
@@ -917,6 +951,8 @@ int32_t sr_keep_count(int32_t b, double alpha) {
 sr_status sr_workspace_size(const sr_model* gen, const sr_model* rm, int32_t prompt_len,
                             const sr_params* p, size_t* bytes) {
   return guard([&] {
+    sr_model stand_in;
+    rm = reward_model_of(gen, rm, p, &stand_in);
     check_pair(gen, rm);
     check_params(p, gen);
     SR_REQUIRE(prompt_len >= 1, SR_ERR_INVALID_ARG, "prompt_len must be >= 1");
@@ -933,6 +969,8 @@ sr_status sr_generate(const sr_model* gen, const sr_model* rm, const int32_t* pr
                       const sr_params* p, void* workspace, size_t ws_bytes, void* stream,
                       int32_t* out_tokens, sr_result* out, sr_trace* trace) {
   return guard([&] {
+    sr_model stand_in;
+    rm = reward_model_of(gen, rm, p, &stand_in);
     check_pair(gen, rm);
     check_params(p, gen);
     check_prompt(prompt, prompt_len, gen->cfg.vocab);

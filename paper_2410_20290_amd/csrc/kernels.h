@@ -128,6 +128,15 @@ struct SampleArgs {
 };
 void sample(const SampleArgs& a, hipStream_t s);
 
+// Probability-as-reward (section 5.3): for every row sampled at `step`
+// (len[r] == step + 1), lp_sum[cand[r]] += ln softmax(logits row)[tok[r]]
+// at temperature 1 (fixed-order fp32 reductions).
+void logprob_accumulate(const float* logits, int64_t row_stride, int rows, int vocab, const int32_t* cand,
+                        const int32_t* tok, const int32_t* len, int step, float* lp_sum, hipStream_t s);
+// score[r] = lp_sum[cand[r]] / len[r] (0 for an empty response).
+void logprob_scores(const float* lp_sum, const int32_t* cand, const int32_t* len, int rows, float* score,
+                    hipStream_t s);
+
 // ---- the cut ------------------------------------------------------------------
 // accept[i] = rank of (score[i] desc, cand[i] asc, NaN lowest) < keep.
 void select_topk(const float* score, const int32_t* cand, int b, int keep, int32_t* accept,

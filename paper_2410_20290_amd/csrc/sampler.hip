@@ -247,4 +247,59 @@ void sample(const SampleArgs& a, hipStream_t s) {
   SR_CHECK_LAUNCH();
 }
 
+// ---------------------------------------------- probability as the reward
+// ln p(tok) = (l_tok - m) - ln sum_i exp(l_i - m), one block per row, sums in
+// a fixed order (per thread over a strided range, then the wave butterfly,
+// then the waves in order).
+__global__ void __launch_bounds__(256)
+logprob_kernel(const float* __restrict__ logits, int64_t row_stride, int vocab, const int32_t* __restrict__ cand,
+               const int32_t* __restrict__ tok, const int32_t* __restrict__ len, int step,
+               float* __restrict__ lp_sum) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  if (len[r] != step + 1) return;  // uniform per block: the row was not sampled at this step
+  const float* lg = logits + (int64_t)r * row_stride;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float mv = -INFINITY;
+  for (int i = tid; i < vocab; i += 256) mv = fmaxf(mv, lg[i]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mv = fmaxf(mv, __shfl_xor(mv, o, 64));
+  if (lane == 0) red[wave] = mv;
+  __syncthreads();
+  const float m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  float sum = 0.f;
+  for (int i = tid; i < vocab; i += 256) sum += expf(lg[i] - m);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+  if (lane == 0) red[wave] = sum;
+  __syncthreads();
+  if (tid == 0) {
+    const float tot = ((red[0] + red[1]) + red[2]) + red[3];
+    lp_sum[cand[r]] += (lg[tok[r]] - m) - logf(tot);
+  }
+}
+
+__global__ void logprob_score_kernel(const float* __restrict__ lp_sum, const int32_t* __restrict__ cand,
+                                     const int32_t* __restrict__ len, int rows, float* __restrict__ score) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r < rows) score[r] = len[r] > 0 ? lp_sum[cand[r]] / (float)len[r] : 0.f;
+}
+
+void logprob_accumulate(const float* logits, int64_t row_stride, int rows, int vocab, const int32_t* cand,
+                        const int32_t* tok, const int32_t* len, int step, float* lp_sum, hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(logprob_kernel, dim3(rows), dim3(256), 0, s, logits, row_stride, vocab, cand, tok, len, step,
+                     lp_sum);
+  SR_CHECK_LAUNCH();
+}
+
+void logprob_scores(const float* lp_sum, const int32_t* cand, const int32_t* len, int rows, float* score,
+                    hipStream_t s) {
+  if (rows <= 0) return;
+  hipLaunchKernelGGL(logprob_score_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, lp_sum, cand, len, rows,
+                     score);
+  SR_CHECK_LAUNCH();
+}
+
 }  // namespace sr

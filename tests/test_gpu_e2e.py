@@ -17,12 +17,13 @@ from oracle import specrej
 pytestmark = pytest.mark.gpu
 
 
-def gpu_run(name, **over):
+def gpu_run(name, reward_kind=0, **over):
     torch, sr = need_gpu()
     c, gen, rm, prompt = device_models(name)
     c = c.with_(**over)
-    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id, c.max_rounds)
-    out = sr.generate(gen, rm, prompt, p, trace=True)
+    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id, c.max_rounds,
+                       reward_kind=reward_kind)
+    out = sr.generate(gen, None if reward_kind else rm, prompt, p, trace=True)
     return c, prompt, out
 
 
@@ -118,3 +119,27 @@ def test_bf16_audit(name):
     mem = [k for k in range(c.n) if not np.isnan(fs[k])]
     refs = np.array([orm.score(list(prompt) + t["all_tokens"][k, : t["all_len"][k]].tolist()) for k in mem])
     assert np.abs(fs[mem] - refs).max() <= tol(c) * np.abs(refs).max()
+
+
+@pytest.mark.parametrize("over", [{}, {"eos_id": 2}, {"n": 40, "alpha": 0.1, "tau": 4, "max_new_tokens": 24}])
+def test_tiny_fp32_logprob_reward_matches_full_oracle(over):
+    """Probability as the reward (section 5.3), no reward model: the GPU's
+    candidates, cuts and answer equal the oracle's run with the mean
+    log-probability score."""
+    say(f"tiny_fp32 logprob e2e {over}")
+    c, prompt, out = gpu_run("tiny_fp32", reward_kind=1, **over)
+    rounds = check_trace_logic(c, out)
+    g, _ = oracle_models("tiny_fp32")
+    lp = lambda pr, toks: specrej.mean_logprob(g, pr, toks)
+    ref = specrej.speculative_rejection(g, None, prompt, c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature,
+                                        c.sample_seed, c.eos_id, c.max_rounds, score_fn=lp)
+    t = out["trace"]
+    for k in range(c.n):
+        assert t["all_tokens"][k, : t["all_len"][k]].tolist() == ref["responses"][k], k
+    assert [(L, b, K) for (L, b, K, *_rest) in rounds] == [r[:3] for r in ref["rounds"]]
+    for (L, b, K, cand, scores, acc), (rL, rb, rK, racc, rsc) in zip(rounds, ref["rounds"]):
+        want = np.array([rsc[k] for k in cand])
+        assert np.abs(scores - want).max() <= 1e-4 * np.abs(want).max()
+        assert sorted(k for k, a in zip(cand, acc) if a) == sorted(racc)
+    assert out["best_index"] == ref["best"] and out["tokens"] == ref["tokens"]
+    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * max(1.0, abs(ref["score"]))

@@ -4,11 +4,13 @@ ceil((1 - alpha) b) by partial reward (section 4.2), the answer is the best
 completed candidate (eq. output), the worked example of section 4.1, the
 memory-budget schedule's closed forms, and brute force on a 2-token toy."""
 import json
+import math
 import os
 from collections import Counter
 
 import numpy as np
 import pytest
+import torch
 from scipy import stats
 
 import synth
@@ -293,3 +295,27 @@ def test_toy_speculative_rejection(toy):
     # every member of I is a full path whose final reward is the enumerated one
     for k in res["final"]:
         assert res["final"][k] == np.float32(reward[tuple(res["responses"][k])])
+
+
+@pytest.mark.slow
+def test_toy_mean_logprob_is_normalised_and_matches_cached_decode(toy):
+    """Section 5.3 score: exp(len * score) over all 2^8 full paths sums to
+    one; the score of every prefix equals the per-step log-probabilities
+    from the KV-cached decode path (a separate code path of the oracle);
+    and one step matches torch's log_softmax."""
+    g, rm, prompt, prob, logp, reward = toy
+    paths = list(prob)
+    total = sum(math.exp(TOY_LMAX * specrej.mean_logprob(g, prompt, list(p))) for p in paths)
+    assert abs(total - 1.0) < 1e-9
+    for p in paths[::37]:
+        state, l0 = g.start(prompt, 1, len(prompt) + TOY_LMAX + 1)
+        lg, acc = l0, 0.0
+        for t, tok in enumerate(p):
+            row = np.asarray(lg).reshape(-1)
+            acc += row[tok] - (row.max() + math.log(np.exp(row - row.max()).sum()))
+            assert specrej.mean_logprob(g, prompt, list(p[:t + 1])) == pytest.approx(acc / (t + 1), abs=1e-12)
+            lg = g.step(state, [tok])[0]
+    lg = g.logits(prompt + [1, 0])[len(prompt) + 1]
+    ref = torch.log_softmax(torch.from_numpy(lg), dim=0).numpy()
+    got = specrej.mean_logprob(g, prompt, [1, 0, 1]) * 3 - specrej.mean_logprob(g, prompt, [1, 0]) * 2
+    assert got == pytest.approx(ref[1], abs=1e-12)
