@@ -108,6 +108,9 @@ def main():
     ap.add_argument("--reward", choices=["model", "logprob"], default="model",
                     help="partial reward: the reward model, or the generator's mean log-probability "
                          "(section 5.3, no reward model)")
+    ap.add_argument("--reward-recompute", action="store_true",
+                    help="run whole responses through the reward model at every decision instead of keeping "
+                         "the survivors' reward-model K/V across rounds")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the hot path is one GPU's batch of "
@@ -139,15 +142,16 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
 
+    rrc = 1 if args.reward_recompute else 0
     p = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                       cfg.eos_id, 0, 0, kind)
+                       cfg.eos_id, 0, 0, kind, rrc)
     ws = sr.Workspace(gen, rm, len(prompt), p)
     log(f"[bench] workspace {ws.nbytes / 2**30:.2f} GiB")
     for i in range(args.warmup):
         o = sr.generate(gen, rm, prompt, p, ws)
         log(f"[bench] warmup {i}: {o['sec_total']:.3f}s generated={o['generated_tokens']}")
     pp = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                        cfg.eos_id, 0, args.profile_every, kind)
+                        cfg.eos_id, 0, args.profile_every, kind, rrc)
     kern = {}
     gen_tokens = 0
     results = []
@@ -173,7 +177,7 @@ def main():
     bon = None
     if not args.no_bon and cfg.alpha > 0:
         pb = sr.make_params(cfg.n, 0.0, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
-                            cfg.eos_id, 0, 0, kind)
+                            cfg.eos_id, 0, 0, kind, rrc)
         wsb = sr.Workspace(gen, rm, len(prompt), pb)
         torch.cuda.synchronize()
         tb = time.perf_counter()
@@ -225,6 +229,8 @@ def main():
                                + f", prompt {cfg.prompt_len}, "
                                f"N={cfg.n}, tau={cfg.tau}, alpha={cfg.alpha}, {cfg.max_new_tokens} new tokens",
                    "reward": args.reward,
+                   "reward_kv": "recomputed each round" if (args.reward_recompute or kind != sr.SR_REWARD_MODEL)
+                                else "cached across rounds",
                    "N": cfg.n, "alpha": cfg.alpha, "tau": cfg.tau, "max_new_tokens": cfg.max_new_tokens,
                    "prompt_len": cfg.prompt_len},
         "s_per_prompt": round(s_per_prompt, 4),

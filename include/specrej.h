@@ -109,7 +109,16 @@ typedef struct {
  *               SR_REWARD_LOGPROB: s(y) = (1/len(y)) ln p(y | x) under the
  *               generator's own softmax at temperature 1 (section 5.3),
  *               accumulated during sampling; `rm` is not evaluated and may
- *               be NULL. */
+ *               be NULL.
+ *  reward_recompute  with the reward model and a schedule that scores more
+ *               than once: 0 = the reward model's keys/values of the
+ *               survivors' responses stay in the workspace across rounds
+ *               (compacted at each cut like the generator's) and a decision
+ *               runs only the tokens generated since the previous one; the
+ *               workspace then holds two more pools of the generator pools'
+ *               slot counts.  1 = every decision runs the whole responses
+ *               through the reward model again.  Both give the same scores up
+ *               to floating-point rounding order. */
 enum { SR_REWARD_MODEL = 0, SR_REWARD_LOGPROB = 1 };
 typedef struct {
   int32_t n;
@@ -121,6 +130,7 @@ typedef struct {
   int32_t max_rounds;
   int32_t profile_every;
   int32_t reward_kind;
+  int32_t reward_recompute;
 } sr_params;
 
 /* Kernel classes of sr_result.kernel_*. */
@@ -279,6 +289,25 @@ sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, 
                               void *stream);
 size_t sr_decode_attention_scratch(int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
                                    int32_t rows, int32_t P, int32_t lt);
+
+/* Causal prefill attention of `rows` rows of lr new tokens each, which follow
+ * t0 tokens of the same row whose keys/values are already cached (the
+ * reward model's scoring pass over the tokens generated since the previous
+ * decision, section 4.2; t0 = 0 scores whole responses).  New token t of row
+ * r sits at row position t0 + t; its query q[r*lr + t][j] (DEVICE float
+ * [rows*lr][n_heads][head_dim]) attends, for KV head
+ * floor(j * n_kv_heads / n_heads), the shared prefix kpre/vpre (DEVICE dtype
+ * [n_kv_heads][P][head_dim]) and the row's own keys/values 0..t0 + t in
+ * kown/vown (DEVICE dtype [rows][n_kv_heads][cap][head_dim]; positions
+ * t0..t0+lr-1 are the new tokens' own, written by the caller);
+ * out[r*lr + t][j*head_dim + d] (DEVICE dtype [rows*lr][n_heads*head_dim]) =
+ * sum_k softmax_k(q . key_k / sqrt(head_dim)) value_k[d].  t0 + lr <= cap,
+ * head_dim in {32, 64, 128}, n_heads / n_kv_heads in {1,2,4,8}; bf16 with
+ * head_dim 128 runs on the matrix cores.  No scratch.  Asynchronous. */
+sr_status sr_prefill_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                               int32_t rows, int32_t lr, const float *q, const void *kpre,
+                               const void *vpre, int32_t P, const void *kown, const void *vown,
+                               int32_t cap, int32_t t0, void *out, void *stream);
 
 /* Teacher-forced generator logits through the decode path: all `rows`
  * continue `prompt` (HOST int32 [prompt_len]) with their own tokens

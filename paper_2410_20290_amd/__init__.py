@@ -48,7 +48,7 @@ KERNEL_CLASSES = ["gen_gemm_mfma", "gen_gemm_hbm", "decode_attn", "rm_gemm", "pr
 class sr_params(ctypes.Structure):
     _fields_ = [("n", _i32), ("alpha", _f64), ("tau", _i32), ("max_new_tokens", _i32),
                 ("temperature", _f32), ("seed", _u64), ("eos_id", _i32), ("max_rounds", _i32),
-                ("profile_every", _i32), ("reward_kind", _i32)]
+                ("profile_every", _i32), ("reward_kind", _i32), ("reward_recompute", _i32)]
 
 
 class sr_result(ctypes.Structure):
@@ -105,7 +105,9 @@ def lib():
                                           _vp, _vp, ctypes.c_size_t, _vp]
         L.sr_decode_attention_scratch.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32]
         L.sr_decode_attention_scratch.restype = ctypes.c_size_t
-        for f in ("sr_projection", "sr_decode_attention", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
+        L.sr_prefill_attention.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
+                                           _i32, _vp, _vp]
+        for f in ("sr_projection", "sr_decode_attention", "sr_prefill_attention", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
                   "sr_logits_teacher_forced", "sr_reward_scores"):
             getattr(L, f).restype = _i32
         _lib = L
@@ -173,9 +175,9 @@ SR_REWARD_MODEL, SR_REWARD_LOGPROB = 0, 1
 
 
 def make_params(n, alpha, tau, max_new_tokens, temperature=1.0, seed=42, eos_id=-1, max_rounds=0,
-                profile_every=0, reward_kind=SR_REWARD_MODEL) -> sr_params:
+                profile_every=0, reward_kind=SR_REWARD_MODEL, reward_recompute=0) -> sr_params:
     return sr_params(n, alpha, tau, max_new_tokens, temperature, seed, eos_id, max_rounds, profile_every,
-                     reward_kind)
+                     reward_kind, reward_recompute)
 
 
 def workspace_size(gen: DeviceModel, rm: DeviceModel, prompt_len: int, p: sr_params) -> int:
@@ -283,6 +285,20 @@ def decode_attention(q, kpre, vpre, ktail, vtail, lt: int, out, stream=None):
     _check(lib().sr_decode_attention(dtype, hd, hq, hkv, rows, _ptr(q), _ptr(kpre), _ptr(vpre), P, _ptr(ktail),
                                      _ptr(vtail), cap, lt, _ptr(out), _ptr(part), need, _stream(stream)))
     return part
+
+
+def prefill_attention(q, kpre, vpre, kown, vown, t0: int, out, stream=None):
+    """sr_prefill_attention: q float [rows][lr][hq][hd]; kpre/vpre [hkv][P][hd]
+    (or None when P = 0); kown/vown [rows][hkv][cap][hd] holding each row's
+    positions 0..t0+lr-1; out [rows][lr][hq*hd] in the model dtype (bf16
+    tensors travel as int16).  See the header."""
+    import torch
+    rows, lr, hq, hd = q.shape
+    hkv, cap = kown.shape[1], kown.shape[2]
+    P = 0 if kpre is None else kpre.shape[1]
+    dtype = SR_BF16 if kown.dtype in (torch.int16, torch.bfloat16) else SR_F32
+    _check(lib().sr_prefill_attention(dtype, hd, hq, hkv, rows, lr, _ptr(q), _ptr(kpre), _ptr(vpre), P, _ptr(kown),
+                                      _ptr(vown), cap, t0, _ptr(out), _stream(stream)))
 
 
 def logits_teacher_forced(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, tokens, ws: Workspace,

@@ -411,9 +411,9 @@ static int tail_mfma_kps(int rows, int hkv, int keys) {
 template <int G, bool PREFIX_ONLY>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
-                                         const bf16_t* __restrict__ vown, int lr, int hq, int hkv,
-                                         bf16_t* __restrict__ out, float qscale, float* __restrict__ part,
-                                         int part_splits);
+                                         const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq,
+                                         int hkv, bf16_t* __restrict__ out, float qscale,
+                                         float* __restrict__ part, int part_splits);
 
 // Whether the shared prefix is attended by the batched MFMA kernel.
 static int prefix_mfma_min_rows() {
@@ -474,7 +474,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     if (pre) {
       hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits),
                          dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr,
-                         nullptr, a.rows, a.hq, a.hkv, nullptr, qscale, a.part, splits);
+                         nullptr, a.rows, 0, 0, a.hq, a.hkv, nullptr, qscale, a.part, splits);
       SR_CHECK_LAUNCH();
     }
     if (tsplits > 0) launch_tail_mfma<G>(a, key0, kps, tsplits, splits, psplits, qscale, s);
@@ -495,7 +495,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
     hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits), dim3(64 * G),
                        0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows,
-                       a.hq, a.hkv, nullptr, qscale, a.part, splits);
+                       0, 0, a.hq, a.hkv, nullptr, qscale, a.part, splits);
     SR_CHECK_LAUNCH();
     if (tsplits > 0) {
       hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
@@ -559,8 +559,8 @@ void decode_attn(const DecodeAttnArgs& a, hipStream_t s) {
 template <typename T, int HD, int G>
 __global__ void __launch_bounds__(256)
 prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, const T* __restrict__ vpre,
-                    int P, const T* __restrict__ kown, const T* __restrict__ vown, int lr, int hq,
-                    int hkv, T* __restrict__ out, float qscale) {
+                    int P, const T* __restrict__ kown, const T* __restrict__ vown, int lr, int cap, int t0,
+                    int hq, int hkv, T* __restrict__ out, float qscale) {
   constexpr int TPQ = 4, DPT = HD / TPQ, QB = 64 / G, KT = 32;
   constexpr int EPL = Vec16<T>::N, CPR = HD / EPL;
   __shared__ float Ks[KT][HD];
@@ -579,11 +579,11 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
   }
   float m = -INFINITY, l = 0.f;
   const int tlast = min(lr, (qb + 1) * QB) - 1;
-  const int nkeys = P + tlast + 1;
+  const int nkeys = P + t0 + tlast + 1;
   const T* kp = kpre + (int64_t)h * P * HD;
   const T* vp = vpre + (int64_t)h * P * HD;
-  const T* ko = kown + ((int64_t)row * hkv + h) * lr * HD;
-  const T* vo = vown + ((int64_t)row * hkv + h) * lr * HD;
+  const T* ko = kown + ((int64_t)row * hkv + h) * cap * HD;
+  const T* vo = vown + ((int64_t)row * hkv + h) * cap * HD;
   for (int kb = 0; kb < nkeys; kb += KT) {
     for (int idx = tid; idx < KT * CPR; idx += 256) {
       const int j = idx / CPR, c = idx % CPR;
@@ -615,7 +615,7 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
       d += __shfl_xor(d, 1, 64);
       d += __shfl_xor(d, 2, 64);
       const int key = kb + j;
-      const bool ok = qvalid && key <= P + t;
+      const bool ok = qvalid && key <= P + t0 + t;
       s[j] = ok ? d : -INFINITY;
       mt = fmaxf(mt, s[j]);
     }
@@ -667,8 +667,8 @@ template <int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
-                         const bf16_t* __restrict__ vown, int lr, int hq, int hkv, bf16_t* __restrict__ out,
-                         float qscale, float* __restrict__ part, int part_splits) {
+                         const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq, int hkv,
+                         bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
   constexpr int HD = 128, NT = 64 * G;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * PF_VROW];
@@ -697,11 +697,11 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   float m = -INFINITY, l = 0.f;
   const int tlast = min(lr, (qb + 1) * 16) - 1;
   const int kbeg = PREFIX_ONLY ? blockIdx.z * 64 : 0;
-  const int nkeys = PREFIX_ONLY ? min(P, kbeg + 64) : P + tlast + 1;
+  const int nkeys = PREFIX_ONLY ? min(P, kbeg + 64) : P + t0 + tlast + 1;
   const bf16_t* kp = kpre + (int64_t)h * P * HD;
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
-  const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * lr * HD;
-  const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * lr * HD;
+  const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * cap * HD;
+  const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * cap * HD;
   for (int kb = kbeg; kb < nkeys; kb += PF_KT) {
     // stage K [key][dim] and V^T [dim][key]: 32 keys x 16 chunks of 8 dims
     for (int c = threadIdx.x; c < PF_KT * 16; c += NT) {
@@ -741,7 +741,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = kb + kt * 16 + 4 * fg + i;
-        const bool ok = qvalid && key < nkeys && (PREFIX_ONLY || key <= P + t);
+        const bool ok = qvalid && key < nkeys && (PREFIX_ONLY || key <= P + t0 + t);
         st[kt][i] = ok ? st[kt][i] : -INFINITY;
         mt = fmaxf(mt, st[kt][i]);
       }
@@ -804,8 +804,8 @@ static void launch_prefill(const PrefillAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
   dim3 grid((a.lr + QB - 1) / QB, a.hkv, a.rows);
   hipLaunchKernelGGL((prefill_attn_kernel<T, HD, G>), grid, dim3(256), 0, s, a.q, (const T*)a.kpre,
-                     (const T*)a.vpre, a.P, (const T*)a.kown, (const T*)a.vown, a.lr, a.hq, a.hkv,
-                     (T*)a.out, qscale);
+                     (const T*)a.vpre, a.P, (const T*)a.kown, (const T*)a.vown, a.lr, a.cap, a.t0, a.hq,
+                     a.hkv, (T*)a.out, qscale);
   SR_CHECK_LAUNCH();
 }
 
@@ -835,8 +835,8 @@ static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf(128.f);
   dim3 grid((a.lr + 15) / 16, a.hkv, a.rows);
   hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
-                     (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.hq, a.hkv,
-                     (bf16_t*)a.out, qscale, nullptr, 0);
+                     (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.cap, a.t0,
+                     a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();
 }
 

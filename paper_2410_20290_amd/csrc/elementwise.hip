@@ -319,11 +319,14 @@ void qkv_finalize(int dtype, const float* part, int splits, int rows, int hq, in
 
 template <typename T>
 __global__ void __launch_bounds__(256)
-score_head_kernel(const float* __restrict__ h, int d, int lr, const int32_t* __restrict__ len,
+score_head_kernel(const float* __restrict__ h, int d, int lr, int t0, const int32_t* __restrict__ len,
                   const T* __restrict__ g, const T* __restrict__ w, float eps, float* __restrict__ score) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  const float* x = h + ((int64_t)r * lr + (len[r] - 1)) * d;
+  // the caller guarantees t0 < len[r] <= t0 + lr; the clamp only keeps the
+  // read inside this row's block
+  const int t = min(max(len[r] - 1 - t0, 0), lr - 1);
+  const float* x = h + ((int64_t)r * lr + t) * d;
   float ss = 0.f;
   for (int i = threadIdx.x; i < d; i += 256) ss += x[i] * x[i];
   ss = block_sum256(ss, red);
@@ -334,30 +337,32 @@ score_head_kernel(const float* __restrict__ h, int d, int lr, const int32_t* __r
   if (threadIdx.x == 0) score[r] = dot;
 }
 
-void score_head(int dtype, const float* h, int d, int lr, const int32_t* len, int rows,
+void score_head(int dtype, const float* h, int d, int lr, int t0, const int32_t* len, int rows,
                 const void* g, const void* w, float eps, float* score, hipStream_t s) {
   if (rows <= 0) return;
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(score_head_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, d, lr, len,
+    hipLaunchKernelGGL(score_head_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
                        (const bf16_t*)g, (const bf16_t*)w, eps, score);
   else
-    hipLaunchKernelGGL(score_head_kernel<float>, dim3(rows), dim3(256), 0, s, h, d, lr, len,
+    hipLaunchKernelGGL(score_head_kernel<float>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
                        (const float*)g, (const float*)w, eps, score);
   SR_CHECK_LAUNCH();
 }
 
 __global__ void gather_tokens_kernel(const int32_t* __restrict__ store, int ld, const int32_t* __restrict__ cand,
-                                     const int32_t* __restrict__ len, int lr, int32_t* __restrict__ tokens) {
+                                     const int32_t* __restrict__ len, int t0, int lr,
+                                     int32_t* __restrict__ tokens) {
   const int r = blockIdx.x;
   const int32_t* src = store + (int64_t)cand[r] * ld;
   const int n = len[r];
-  for (int t = threadIdx.x; t < lr; t += blockDim.x) tokens[(int64_t)r * lr + t] = t < n ? src[t] : 0;
+  for (int t = threadIdx.x; t < lr; t += blockDim.x)
+    tokens[(int64_t)r * lr + t] = t0 + t < n ? src[t0 + t] : 0;
 }
 
 void gather_tokens(const int32_t* store, int ld, const int32_t* cand, const int32_t* len, int rows,
-                   int lr, int32_t* tokens, hipStream_t s) {
+                   int t0, int lr, int32_t* tokens, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(gather_tokens_kernel, dim3(rows), dim3(256), 0, s, store, ld, cand, len, lr, tokens);
+  hipLaunchKernelGGL(gather_tokens_kernel, dim3(rows), dim3(256), 0, s, store, ld, cand, len, t0, lr, tokens);
   SR_CHECK_LAUNCH();
 }
 

@@ -96,6 +96,8 @@ static void check_params(const sr_params* p, const sr_model* gen) {
   SR_REQUIRE((int64_t)p->n * p->tau <= (int64_t)1 << 31, SR_ERR_INVALID_ARG, "n * tau too large");
   SR_REQUIRE(p->reward_kind == SR_REWARD_MODEL || p->reward_kind == SR_REWARD_LOGPROB, SR_ERR_INVALID_ARG,
              "reward_kind must be SR_REWARD_MODEL or SR_REWARD_LOGPROB");
+  SR_REQUIRE(p->reward_recompute == 0 || p->reward_recompute == 1, SR_ERR_INVALID_ARG,
+             "reward_recompute must be 0 or 1");
 }
 
 // The reward model of a run: `rm`, or (log-probability reward without a
@@ -119,6 +121,7 @@ struct Plan {
   int64_t S[2];  // token-slot capacity of pools A and B
   int Tc;        // tokens per reward-model chunk
   size_t gpart, apart;
+  bool rkv;      // the reward model's response K/V is kept across rounds (pools of S[i] slots)
 };
 
 // Decision length for a round that starts with b unfinished candidates after
@@ -151,6 +154,9 @@ static Plan make_plan(const Dims& g, const Dims& rm, int P, const sr_params* p) 
   }
   pl.S[0] = std::max<int64_t>((int64_t)pl.N * D0, after);
   pl.S[1] = after;
+  // A reward-model K/V cache pays off only when some round is scored after
+  // an earlier one, i.e. when the first round can end in a cut.
+  pl.rkv = p->reward_kind == SR_REWARD_MODEL && !p->reward_recompute && can_cut && D0 < pl.Lmax;
   const int64_t want = std::min<int64_t>((int64_t)pl.N * pl.Lmax, 32768);
   pl.Tc = (int)std::max<int64_t>(std::max<int64_t>(want, pl.Lmax), P);
   // GEMM split-K partials over every shape and row count that can occur.
@@ -209,6 +215,7 @@ struct Layout {
   float2 *rope_g, *rope_r;
   void *gpre, *rpre;        // [nl][2][hkv][P][hd]
   void* pool[2];            // [nl][2][S * hkv * hd]
+  void* rpool[2];           // reward model's, same slots (when Plan::rkv)
   int32_t* store;           // [N][Lmax]
   int32_t* cand_len;        // [N]
   State st[3];
@@ -231,6 +238,8 @@ static Layout carve(void* base, const Dims& g, const Dims& rm, const Plan& pl, s
   L.gpre = a.bytes((size_t)g.nl * 2 * g.hkv * P * g.hd * g.es);
   L.rpre = a.bytes((size_t)rm.nl * 2 * rm.hkv * P * rm.hd * rm.es);
   for (int i = 0; i < 2; ++i) L.pool[i] = a.bytes((size_t)g.nl * 2 * pl.S[i] * g.hkv * g.hd * g.es);
+  for (int i = 0; i < 2; ++i)
+    L.rpool[i] = a.bytes(pl.rkv ? (size_t)rm.nl * 2 * pl.S[i] * rm.hkv * rm.hd * rm.es : 0);
   L.store = a.take<int32_t>((size_t)N * Lmax);
   L.cand_len = a.take<int32_t>(N);
   for (int i = 0; i < 3; ++i) {
@@ -387,11 +396,14 @@ static void ffn_block(const Ctx& c, bool decode, const Model& M, int l, float* h
 }
 
 // Prefill of `rows` sequences of `lr` tokens (device tokens [rows][lr]) at
-// positions pos0 + t, attending the shared prefix (P tokens, may be 0) and
-// causally their own tokens.  K/V of layer l are written through kv_out(l).
+// positions pos0 + t, attending the shared prefix `pre` (P tokens, may be 0)
+// and causally their own tokens.  K/V of layer l are written through
+// kv_out(l) as [rows][hkv][cap][hd] at index t0 + t of each row, after t0
+// cached tokens of that row which the attention reads too.  Leaves the final
+// hidden states in L.ch.
 template <typename KvOut>
 static void prefill(const Ctx& c, const Model& M, const float2* rope, const int32_t* tokens, int rows,
-                    int lr, int pos0, const void* pre, int P, KvOut kv_out) {
+                    int lr, int pos0, const void* pre, int P, KvOut kv_out, int cap, int t0) {
   const Dims& m = M.m;
   Layout& L = *c.L;
   const int T = rows * lr;
@@ -403,7 +415,7 @@ static void prefill(const Ctx& c, const Model& M, const float2* rope, const int3
               [&] { rmsnorm(m.dtype, L.ch, m.d, M.attn_norm(l), m.d, m.eps, T, L.cxn, m.d, c.s); });
     run_gemm(c, false, m.dtype, L.cxn, m.d, M.wqkv(l), m.d, T, m.qkv, m.d, EPI_STORE, L.cqkv, m.qkv, 0);
     run_other(c, (double)T * (m.qkv * 4.0 + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
-      rope_scatter(m.dtype, L.cqkv, rows, lr, m.hq, m.hkv, m.hd, rope, pos0, L.cq, kd, vd, lr, 0, c.s);
+      rope_scatter(m.dtype, L.cqkv, rows, lr, m.hq, m.hkv, m.hd, rope, pos0, L.cq, kd, vd, cap, t0, c.s);
     });
     PrefillAttnArgs a;
     a.dtype = m.dtype; a.hd = m.hd; a.hq = m.hq; a.hkv = m.hkv; a.rows = rows; a.lr = lr;
@@ -412,10 +424,11 @@ static void prefill(const Ctx& c, const Model& M, const float2* rope, const int3
     a.kpre = pre ? (const char*)pre + l * lay : nullptr;
     a.vpre = pre ? (const char*)pre + l * lay + lay / 2 : nullptr;
     a.P = pre ? P : 0;
-    a.kown = kd; a.vown = vd; a.out = L.co;
+    a.kown = kd; a.vown = vd; a.cap = cap; a.t0 = t0; a.out = L.co;
     const double Pp = a.P;
-    const double abytes = 2.0 * m.hkv * m.hd * m.es * (Pp + (double)T) + (double)T * m.hq * m.hd * (4 + m.es);
-    const double aflops = 4.0 * m.hq * m.hd * rows * (Pp * lr + 0.5 * lr * (lr + 1.0));
+    const double abytes = 2.0 * m.hkv * m.hd * m.es * (Pp + (double)rows * (t0 + lr)) +
+                          (double)T * m.hq * m.hd * (4 + m.es);
+    const double aflops = 4.0 * m.hq * m.hd * rows * ((Pp + t0) * lr + 0.5 * lr * (lr + 1.0));
     timed(c, SR_K_PREFILL_ATTN, abytes, aflops, [&] { prefill_attn(a, c.s); });
     run_gemm(c, false, m.dtype, L.co, m.hq * m.hd, M.wo(l), m.hq * m.hd, T, m.d, m.hq * m.hd, EPI_RESID,
              L.ch, m.d, 0);
@@ -431,24 +444,40 @@ static void prompt_prefill(const Ctx& c, const Model& M, const float2* rope, voi
   prefill(c, M, rope, c.L->ctok, 1, P, 0, nullptr, 0, [&](int l, void** k, void** v) {
     *k = (char*)pre + l * lay;
     *v = (char*)pre + l * lay + lay / 2;
-  });
+  }, P, 0);
 }
 
 // Reward scores of `rows` rows (cand/len arrays of a state) at max length lr.
+// Without a cache (pool == nullptr) the whole responses are run through the
+// reward model.  With one, row r's K/V of response positions 0..t0-1 are in
+// the pool ([nl][2] blocks of pool_block elements, rows of cap positions),
+// every row has t0 < len <= lr, and only positions t0..lr-1 are run, their
+// K/V appended to the pool.
 static void reward_rows(const Ctx& c, const Model& R, const int32_t* cand, const int32_t* len, int rows,
-                        int lr, float* score) {
+                        int lr, float* score, int t0 = 0, void* pool = nullptr, int64_t pool_block = 0,
+                        int cap = 0) {
   const Plan& pl = *c.pl;
   Layout& L = *c.L;
-  const int per = std::max(1, pl.Tc / lr);
+  const Dims& m = R.m;
+  SR_REQUIRE(pool || t0 == 0, SR_ERR_INTERNAL, "reward prefix without a cache");
+  const int nl = lr - t0;
+  const int per = std::max(1, pl.Tc / nl);
   for (int r0 = 0; r0 < rows; r0 += per) {
     const int rc = std::min(per, rows - r0);
-    run_other(c, (double)rc * lr * 8, [&] { gather_tokens(L.store, pl.Lmax, cand + r0, len + r0, rc, lr, L.ctok, c.s); });
-    prefill(c, R, L.rope_r, L.ctok, rc, lr, pl.P, L.rpre, pl.P, [&](int, void** k, void** v) {
-      *k = L.ck;
-      *v = L.cv;
-    });
-    run_other(c, (double)rc * R.m.d * 4, [&] {
-      score_head(R.m.dtype, L.ch, R.m.d, lr, len + r0, rc, R.w->final_norm, R.w->head, R.m.eps, score + r0, c.s);
+    run_other(c, (double)rc * nl * 8,
+              [&] { gather_tokens(L.store, pl.Lmax, cand + r0, len + r0, rc, t0, nl, L.ctok, c.s); });
+    const size_t row0 = (size_t)r0 * m.hkv * cap * m.hd;
+    prefill(c, R, L.rope_r, L.ctok, rc, nl, pl.P + t0, L.rpre, pl.P, [&](int l, void** k, void** v) {
+      if (pool) {
+        *k = (char*)pool + ((size_t)(2 * l) * pool_block + row0) * m.es;
+        *v = (char*)pool + ((size_t)(2 * l + 1) * pool_block + row0) * m.es;
+      } else {
+        *k = L.ck;
+        *v = L.cv;
+      }
+    }, pool ? cap : nl, t0);
+    run_other(c, (double)rc * m.d * 4, [&] {
+      score_head(m.dtype, L.ch, m.d, nl, t0, len + r0, rc, R.w->final_norm, R.w->head, m.eps, score + r0, c.s);
     });
   }
 }
@@ -606,10 +635,14 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   const int N = pl.N, Lmax = pl.Lmax;
   std::memset(out, 0, sizeof(*out));
   // partial rewards of the rows of a round: the reward model, or the mean
-  // log-probability accumulated while sampling (section 5.3)
-  auto score_rows = [&](const State& st, int b, int D) {
+  // log-probability accumulated while sampling (section 5.3).  With the
+  // reward model's cache, the survivors of the last cut bring their K/V of
+  // the first t0 response tokens.
+  auto score_rows = [&](const State& st, int b, int D, int cur, int cap, int t0) {
     if (lp_mode) {
       logprob_scores(L.lp_sum, st.cand, st.len, b, L.score, s);
+    } else if (pl.rkv) {
+      reward_rows(c, R, st.cand, st.len, b, D, L.score, t0, L.rpool[cur], pl.S[cur] * rd.hkv * rd.hd, cap);
     } else {
       reward_rows(c, R, st.cand, st.len, b, D, L.score);
     }
@@ -638,6 +671,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   int b = N, r = 0, step = 0;
   int D = decision(pl, b, r);
   int cap = D;
+  int t0 = 0;  // response tokens whose reward-model K/V the cache holds
   int64_t generated = 0;
   std::vector<int32_t> h_done, h_i32(N);
   std::vector<float> h_f32(N);
@@ -675,7 +709,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     if (D == Lmax || unfinished == 0) {
       // every candidate of this round is complete: score all, all join I
       tph.start();
-      score_rows(st, b, D);
+      score_rows(st, b, D, cur, cap, t0);
       out->sec_reward += tph.stop();
       CutArgs ca;
       std::memset(&ca, 0, sizeof(ca));
@@ -694,7 +728,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     const int K = keep_of(b, pl.appm);
     SR_REQUIRE(K < b, SR_ERR_INTERNAL, "decision point without a possible rejection");
     tph.start();
-    score_rows(st, b, D);
+    score_rows(st, b, D, cur, cap, t0);
     out->sec_reward += tph.stop();
     tph.start();
     const int nxt = 1 - cur;
@@ -792,11 +826,21 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     ka.cap_src = cap; ka.cap_dst = nD; ka.len = step - 1;
     timed(c, SR_K_CUT, 4.0 * gd.nl * cnt * (double)(step - 1) * gd.hkv * gd.hd * gd.es, 0.0,
           [&] { compact(ka, s); });
+    if (pl.rkv) {
+      // the reward model's K/V of all `step` response tokens moves the same way
+      CompactArgs kr = ka;
+      kr.src = L.rpool[cur]; kr.src_block = pl.S[cur] * rd.hkv * rd.hd;
+      kr.dst = L.rpool[nxt]; kr.dst_block = pl.S[nxt] * rd.hkv * rd.hd;
+      kr.n_layers = rd.nl; kr.hkv = rd.hkv; kr.hd = rd.hd; kr.elem_bytes = rd.es; kr.len = step;
+      timed(c, SR_K_CUT, 4.0 * rd.nl * cnt * (double)step * rd.hkv * rd.hd * rd.es, 0.0,
+            [&] { compact(kr, s); });
+    }
     SR_HIP(hipMemsetAsync(ns.done, 0, sizeof(int32_t) * cnt, s));
     out->sec_cut += tph.stop();
     prof.flush();
     cur = nxt;
     b = cnt;
+    t0 = step;
     D = nD;
     cap = nD;
   }
@@ -1100,6 +1144,29 @@ sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, 
     a.kpre = kpre; a.vpre = vpre; a.P = P; a.ktail = ktail; a.vtail = vtail; a.cap = cap; a.lt = lt;
     a.out = out; a.part = scratch; a.part_cap = scratch_elems;
     decode_attn(a, (hipStream_t)stream);
+  });
+}
+
+sr_status sr_prefill_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads, int32_t rows,
+                               int32_t lr, const float* q, const void* kpre, const void* vpre, int32_t P,
+                               const void* kown, const void* vown, int32_t cap, int32_t t0, void* out,
+                               void* stream) {
+  return guard([&] {
+    SR_REQUIRE(dtype == SR_F32 || dtype == SR_BF16, SR_ERR_INVALID_ARG, "unknown dtype");
+    SR_REQUIRE(head_dim == 32 || head_dim == 64 || head_dim == 128, SR_ERR_UNSUPPORTED,
+               "head_dim must be 32, 64 or 128");
+    SR_REQUIRE(n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0, SR_ERR_INVALID_ARG, "bad head counts");
+    const int g = n_heads / n_kv_heads;
+    SR_REQUIRE(g == 1 || g == 2 || g == 4 || g == 8, SR_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8");
+    SR_REQUIRE(rows >= 0 && lr >= 0 && P >= 0 && t0 >= 0 && (int64_t)t0 + lr <= cap, SR_ERR_INVALID_ARG,
+               "bad rows / lr / P / t0 / cap");
+    if (rows == 0 || lr == 0) return;
+    SR_REQUIRE(q && out && kown && vown && (P == 0 || (kpre && vpre)), SR_ERR_INVALID_ARG, "NULL buffer");
+    PrefillAttnArgs a;
+    a.dtype = dtype; a.hd = head_dim; a.hq = n_heads; a.hkv = n_kv_heads; a.rows = rows; a.lr = lr;
+    a.q = q; a.kpre = kpre; a.vpre = vpre; a.P = P; a.kown = kown; a.vown = vown; a.cap = cap; a.t0 = t0;
+    a.out = out;
+    prefill_attn(a, (hipStream_t)stream);
   });
 }
 

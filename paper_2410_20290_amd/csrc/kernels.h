@@ -55,12 +55,13 @@ void rope_table(float2* tab, int npos, int hd, double theta, hipStream_t s);
 void rope_scatter(int dtype, const float* qkv, int rows, int lr, int hq, int hkv, int hd,
                   const float2* tab, int pos0, float* qout, void* kdst, void* vdst, int cap,
                   int t0, hipStream_t s);
-// score[r] = w . RMSNorm(h[r*lr + len[r]-1]) * g  (fused reward head).
-void score_head(int dtype, const float* h, int d, int lr, const int32_t* len, int rows,
+// score[r] = w . RMSNorm(h[r*lr + len[r]-1-t0]) * g  (fused reward head;
+// h holds response positions t0..t0+lr-1 of each row, t0 < len[r] <= t0+lr).
+void score_head(int dtype, const float* h, int d, int lr, int t0, const int32_t* len, int rows,
                 const void* g, const void* w, float eps, float* score, hipStream_t s);
-// tokens[r][t] = t < len[r] ? store[cand[r]][t] : 0 for t < lr (store row stride ld).
+// tokens[r][t] = t0+t < len[r] ? store[cand[r]][t0+t] : 0 for t < lr (store row stride ld).
 void gather_tokens(const int32_t* store, int ld, const int32_t* cand, const int32_t* len, int rows,
-                   int lr, int32_t* tokens, hipStream_t s);
+                   int t0, int lr, int32_t* tokens, hipStream_t s);
 void philox_fill(uint64_t seed, const uint32_t* ctr, int n, uint32_t* out, hipStream_t s);
 // h[r] = E[tok[r]] (fp32); xn[r] = RMSNorm(h[r]) * g (model dtype).
 void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, const void* g, float eps,
@@ -93,15 +94,18 @@ struct DecodeAttnArgs {
 int decode_attn_splits(int rows, int hkv, int keys);
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s);
 
-// Prefill: rows of lr tokens; token (r, t) attends the shared prefix
-// kpre/vpre [hkv][P][hd] and its row's own keys 0..t in kown/vown
-// [r][hkv][lr][hd].  q fp32 [rows*lr][hq][hd]; out [rows*lr][hq*hd].
+// Prefill: rows of lr new tokens that follow t0 tokens already cached for
+// their row; new token (r, t) sits at response position t0 + t and attends
+// the shared prefix kpre/vpre [hkv][P][hd] and its row's own keys
+// 0..t0 + t in kown/vown [r][hkv][cap][hd] (cap >= t0 + lr).
+// q fp32 [rows*lr][hq][hd]; out [rows*lr][hq*hd].
 struct PrefillAttnArgs {
   int dtype, hd, hq, hkv, rows, lr;
   const float* q;
   const void *kpre, *vpre;
   int P;
   const void *kown, *vown;
+  int cap = 0, t0 = 0;
   void* out;
 };
 void prefill_attn(const PrefillAttnArgs& a, hipStream_t s);

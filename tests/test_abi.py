@@ -30,7 +30,7 @@ def declared_symbols():
 
 def test_header_symbols_exported(L):
     names = declared_symbols()
-    assert len(names) == 14, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -72,10 +72,35 @@ def test_workspace_size_of_every_config(L, name):
         assert n0 < 300 * 2**30
 
 
+def test_reward_cache_size():
+    """The reward model's cache of the 8B-shaped pair adds two pools of the
+    generator pools' slot counts (N * tau = 65536 slots each at N=512,
+    tau=128, alpha=0.8) and nothing when it cannot be used."""
+    c = synth.CONFIGS["8b_bf16"]
+    gen, rm = fake_model(c.model, False), fake_model(c.model, True)
+    kvb = 2 * 32 * 8 * 128 * 2
+    sizes = {}
+    for rc in (0, 1):
+        st, sizes[rc] = ws_size(sr.lib(), gen, rm, c.prompt_len,
+                                sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, reward_recompute=rc))
+        assert st == sr.SR_OK
+    assert abs(sizes[0] - sizes[1] - 2 * c.n * c.tau * kvb) <= 4096
+    # Best-of-N scores once: no cache whatever the flag
+    b = [ws_size(sr.lib(), gen, rm, c.prompt_len, sr.make_params(c.n, 0.0, c.tau, c.max_new_tokens,
+                                                                 reward_recompute=rc))[1] for rc in (0, 1)]
+    assert b[0] == b[1]
+    # the log-probability reward has no reward model to cache
+    b = [ws_size(sr.lib(), gen, rm, c.prompt_len, sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens,
+                                                                 reward_kind=sr.SR_REWARD_LOGPROB,
+                                                                 reward_recompute=rc))[1] for rc in (0, 1)]
+    assert b[0] == b[1]
+
+
 BAD_PARAMS = [
     dict(n=0), dict(n=5000), dict(alpha=1.0), dict(alpha=-0.1), dict(alpha=float("nan")), dict(tau=0),
     dict(max_new_tokens=0), dict(temperature=-1.0), dict(temperature=float("inf")), dict(eos_id=512),
-    dict(eos_id=-2), dict(max_rounds=-1),
+    dict(eos_id=-2), dict(max_rounds=-1), dict(reward_kind=2), dict(reward_recompute=2),
+    dict(reward_recompute=-1),
 ]
 
 
@@ -143,3 +168,15 @@ def test_kernel_entries_reject_bad_arguments(L):
     assert a(sb=64) == sr.SR_ERR_INVALID_ARG
     assert a(dst=0x100100) == sr.SR_ERR_INVALID_ARG
     assert a(b=0) == sr.SR_ERR_INVALID_ARG
+    # prefill attention: cached + new positions beyond the row capacity, shapes
+    pa = lambda **k: L.sr_prefill_attention(k.get("dt", sr.SR_BF16), k.get("hd", 128), k.get("hq", 8),
+                                            k.get("hkv", 2), k.get("rows", 2), k.get("lr", 4), 0x1000, 0x2000,
+                                            0x3000, 16, 0x4000, 0x5000, k.get("cap", 8), k.get("t0", 4), 0x6000,
+                                            None)
+    assert pa(t0=5) == sr.SR_ERR_INVALID_ARG
+    assert pa(t0=-1) == sr.SR_ERR_INVALID_ARG
+    assert pa(hd=48) == sr.SR_ERR_UNSUPPORTED
+    assert pa(hq=6, hkv=4) == sr.SR_ERR_INVALID_ARG
+    assert pa(hq=6, hkv=2) == sr.SR_ERR_UNSUPPORTED
+    assert pa(dt=7) == sr.SR_ERR_INVALID_ARG
+    assert pa(rows=0) == sr.SR_OK and pa(lr=0) == sr.SR_OK

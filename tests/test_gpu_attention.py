@@ -1,12 +1,13 @@
-"""Decode attention (sr_decode_attention) against the oracle's float64
-decode attention on the same bf16 / fp32 inputs: shared prefix plus each
-row's own tail, ragged tails, no prefix, prefix only, every query-group
+"""Decode attention (sr_decode_attention) and prefill attention
+(sr_prefill_attention) against the oracle's float64 attention on the same
+bf16 / fp32 inputs: shared prefix plus each row's own keys, ragged tails, no
+prefix, prefix only, cached history before the new tokens, every query-group
 size and head size the kernels take."""
 import numpy as np
 import pytest
 
 from gpu_util import need_gpu, say
-from oracle.transformer import decode_attention
+from oracle.transformer import causal_attention, decode_attention
 
 pytestmark = pytest.mark.gpu
 
@@ -68,6 +69,56 @@ def test_decode_attention(dtype, hd, hq, hkv, rows, P, lt, cap):
         k = np.concatenate([kp.transpose(1, 0, 2), kt[r, :, :lt].transpose(1, 0, 2)], axis=0).astype(np.float64)
         v = np.concatenate([vp.transpose(1, 0, 2), vt[r, :, :lt].transpose(1, 0, 2)], axis=0).astype(np.float64)
         ref = decode_attention(q[r].astype(np.float64), k, v, hkv)
+        worst = max(worst, float(np.abs(got[r] - ref).max() / max(1.0, np.abs(ref).max())))
+    tol = 1e-2 if bf16 else 1e-5
+    assert worst <= tol, worst
+
+
+PREFILL_CASES = [
+    # dtype, hd, hq, hkv, rows, P, t0, lr, cap
+    ("bf16", 128, 32, 8, 3, 40, 37, 29, 70),      # matrix-core kernel, ragged tiles
+    ("bf16", 128, 32, 8, 2, 256, 128, 100, 636),  # 8B shapes: second scoring round
+    ("bf16", 128, 8, 8, 2, 0, 16, 33, 49),
+    ("bf16", 128, 16, 2, 2, 17, 0, 50, 64),
+    ("bf16", 128, 32, 8, 1, 5, 0, 1, 1),
+    ("bf16", 64, 8, 2, 3, 33, 20, 17, 40),         # vector kernel
+    ("f32", 32, 4, 4, 2, 5, 9, 11, 20),
+    ("f32", 64, 8, 2, 1, 0, 0, 1, 1),
+    ("f32", 32, 8, 1, 2, 3, 64, 40, 110),
+]
+
+
+@pytest.mark.parametrize("dtype,hd,hq,hkv,rows,P,t0,lr,cap", PREFILL_CASES)
+def test_prefill_attention(dtype, hd, hq, hkv, rows, P, t0, lr, cap):
+    """The new tokens' outputs equal the last lr rows of the causal attention
+    of the whole sequence (prefix, cached tokens, new tokens)."""
+    torch, sr = need_gpu()
+    say(f"prefill attention {dtype} hd={hd} hq={hq} hkv={hkv} rows={rows} P={P} t0={t0} lr={lr} cap={cap}")
+    bf16 = dtype == "bf16"
+    rng = np.random.default_rng(hd + hq + rows + P + t0 + lr)
+    q = rng.normal(size=(rows, lr, hq, hd)).astype(np.float32)
+    kp, vp = rng.normal(size=(2, hkv, P, hd)).astype(np.float32)
+    ko, vo = rng.normal(size=(2, rows, hkv, cap, hd)).astype(np.float32)   # beyond t0 + lr: never read
+    if bf16:
+        kp, vp, ko, vo = (bf16_round(a) for a in (kp, vp, ko, vo))
+    out = torch.zeros((rows, lr, hq * hd), dtype=torch.int16 if bf16 else torch.float32, device="cuda")
+    kpd = to_dev(torch, kp, bf16) if P else None
+    vpd = to_dev(torch, vp, bf16) if P else None
+    sr.prefill_attention(torch.from_numpy(q).cuda(), kpd, vpd, to_dev(torch, ko, bf16), to_dev(torch, vo, bf16), t0,
+                         out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    if bf16:
+        got = (got.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    got = got.reshape(rows, lr, hq, hd)
+    T = P + t0 + lr
+    worst = 0.0
+    for r in range(rows):
+        k = np.concatenate([kp.transpose(1, 0, 2), ko[r, :, :t0 + lr].transpose(1, 0, 2)], axis=0).astype(np.float64)
+        v = np.concatenate([vp.transpose(1, 0, 2), vo[r, :, :t0 + lr].transpose(1, 0, 2)], axis=0).astype(np.float64)
+        qf = np.zeros((T, hq, hd))
+        qf[T - lr:] = q[r]
+        ref = causal_attention(qf, k, v, hkv)[T - lr:]
         worst = max(worst, float(np.abs(got[r] - ref).max() / max(1.0, np.abs(ref).max())))
     tol = 1e-2 if bf16 else 1e-5
     assert worst <= tol, worst

@@ -17,12 +17,12 @@ from oracle import specrej
 pytestmark = pytest.mark.gpu
 
 
-def gpu_run(name, reward_kind=0, **over):
+def gpu_run(name, reward_kind=0, reward_recompute=0, **over):
     torch, sr = need_gpu()
     c, gen, rm, prompt = device_models(name)
     c = c.with_(**over)
     p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id, c.max_rounds,
-                       reward_kind=reward_kind)
+                       reward_kind=reward_kind, reward_recompute=reward_recompute)
     out = sr.generate(gen, None if reward_kind else rm, prompt, p, trace=True)
     return c, prompt, out
 
@@ -84,6 +84,34 @@ def test_tiny_fp32_matches_full_oracle(over):
         assert out["generated_tokens"] == specrej.schedule(c.n, c.alpha, c.tau, c.max_new_tokens, c.max_rounds)[1]
 
 
+@pytest.mark.parametrize("name,over,rtol", [("tiny_fp32", {}, 1e-5), ("tiny_fp32", {"eos_id": 2}, 1e-5),
+                                             ("small_bf16", {}, 2e-2)])
+def test_reward_cache_matches_recompute(name, over, rtol):
+    """Scoring through the reward model's cached K/V of the survivors and
+    re-running whole responses give the same first-round scores bit for bit
+    (the same arithmetic), later-round scores within rounding, and the same
+    run wherever the cuts agree."""
+    say(f"{name} reward cache vs recompute {over}")
+    c, _, a = gpu_run(name, **over)
+    _, _, b = gpu_run(name, reward_recompute=1, **over)
+    ra, rb = trace_rounds(a), trace_rounds(b)
+    assert len(ra) >= 2
+    assert np.array_equal(ra[0][4], rb[0][4])
+    for x, y in zip(ra, rb):
+        if x[:4] != y[:4]:
+            break
+        assert np.abs(x[4] - y[4]).max() <= rtol * np.abs(y[4]).max(), x[0]
+    if [x[:4] for x in ra] == [y[:4] for y in rb] and all(np.array_equal(x[5], y[5]) for x, y in zip(ra, rb)):
+        fa, fb = a["trace"]["final_scores"], b["trace"]["final_scores"]
+        assert np.array_equal(np.isnan(fa), np.isnan(fb))
+        m = ~np.isnan(fa)
+        assert np.abs(fa[m] - fb[m]).max() <= rtol * np.abs(fb[m]).max()
+        assert a["generated_tokens"] == b["generated_tokens"]
+        # the answer agrees unless two members tie within rounding
+        if a["best_index"] != b["best_index"]:
+            assert abs(fb[a["best_index"]] - fb[b["best_index"]]) <= 2 * rtol * np.abs(fb[m]).max()
+
+
 @pytest.mark.parametrize("name", ["small_bf16"])
 def test_bf16_audit(name):
     torch, sr = need_gpu()
@@ -108,12 +136,14 @@ def test_bf16_audit(name):
     for k in (0, c.n // 2, c.n - 1):
         ref = g.logits(list(prompt) + list(toks[k]))[len(prompt) - 1: len(prompt) - 1 + c.tau]
         assert np.abs(lg[k] - ref).max() <= tol(c) * np.abs(ref).max()
-    # (3) partial rewards of the first cut, recomputed by the oracle
-    L0, b0, K0, cand0, sc0, acc0 = rounds[0]
-    for j in (0, 7, b0 - 1):
-        k = cand0[j]
-        ref = orm.score(list(prompt) + t["all_tokens"][k, :L0].tolist())
-        assert abs(sc0[j] - ref) <= tol(c) * max(abs(ref), np.abs(sc0).max())
+    # (3) partial rewards of every cut, recomputed by the oracle (the rounds
+    # after the first score through the reward model's cached K/V)
+    assert len(rounds) >= 2
+    for (L0, b0, K0, cand0, sc0, acc0) in rounds:
+        for j in sorted({0, min(7, b0 - 1), b0 - 1}):
+            k = cand0[j]
+            ref = orm.score(list(prompt) + t["all_tokens"][k, :L0].tolist())
+            assert abs(sc0[j] - ref) <= tol(c) * max(abs(ref), np.abs(sc0).max()), (L0, j)
     # (4) final rewards of I, recomputed by the oracle
     fs = t["final_scores"]
     mem = [k for k in range(c.n) if not np.isnan(fs[k])]
