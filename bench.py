@@ -108,6 +108,9 @@ def main():
     ap.add_argument("--reward", choices=["model", "logprob"], default="model",
                     help="partial reward: the reward model, or the generator's mean log-probability "
                          "(section 5.3, no reward model)")
+    ap.add_argument("--memory-plan", action="store_true",
+                    help="take tau from the device's free memory (Algorithm 1, first step): the largest tau whose "
+                         "workspace fits in the free HBM after the weights, less 4 GiB")
     ap.add_argument("--reward-recompute", action="store_true",
                     help="run whole responses through the reward model at every decision instead of keeping "
                          "the survivors' reward-model K/V across rounds")
@@ -143,12 +146,21 @@ def main():
     log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
 
     rrc = 1 if args.reward_recompute else 0
+    if args.memory_plan:
+        free, _ = torch.cuda.mem_get_info()
+        cap = max(0, free - (4 << 30))
+        q = sr.plan_for_memory(gen, rm, len(prompt), sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens,
+                                                                     reward_kind=kind, reward_recompute=rrc), cap)
+        log(f"[bench] memory plan: {free / 2**30:.1f} GiB free -> tau = {q.tau} at N = {q.n}")
+        cfg = cfg.with_(tau=q.tau)
     p = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
                        cfg.eos_id, 0, 0, kind, rrc)
     ws = sr.Workspace(gen, rm, len(prompt), p)
     log(f"[bench] workspace {ws.nbytes / 2**30:.2f} GiB")
+    warm = None
     for i in range(args.warmup):
-        o = sr.generate(gen, rm, prompt, p, ws)
+        o = sr.generate(gen, rm, prompt, p, ws, trace=i == 0)
+        warm = warm or o
         log(f"[bench] warmup {i}: {o['sec_total']:.3f}s generated={o['generated_tokens']}")
     pp = sr.make_params(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
                         cfg.eos_id, 0, args.profile_every, kind, rrc)
@@ -181,13 +193,30 @@ def main():
         wsb = sr.Workspace(gen, rm, len(prompt), pb)
         torch.cuda.synchronize()
         tb = time.perf_counter()
-        ob = sr.generate(gen, rm, prompt, pb, wsb)
+        ob = sr.generate(gen, rm, prompt, pb, wsb, trace=True)
         torch.cuda.synchronize()
         tb = time.perf_counter() - tb
         bon = {"s_per_prompt": round(tb, 4), "tokens_per_s": round(ob["generated_tokens"] / tb, 1),
                "generated_tokens": ob["generated_tokens"], "best_index": ob["best_index"],
                "sr_best_index": results[-1]["best_index"]}
         log(f"[bench] best-of-N (alpha=0): {tb:.3f}s")
+        if warm is not None and warm["trace"]["rounds"] > 0:
+            # section 5 and Appendix B diagnostics: the first cut's partial
+            # rewards against Best-of-N's final rewards of the same candidates
+            # (the same seed draws the same responses), the answer's reward on
+            # the range of Best-of-N's; values on random weights say nothing
+            # about a trained reward model
+            b0 = int(warm["trace"]["round_b"][0])
+            cand0 = warm["trace"]["round_cand"][0, :b0]
+            partial = warm["trace"]["round_scores"][0, :b0]
+            final = ob["trace"]["final_scores"][cand0]
+            pr, kd = sr.correlation(partial, final)
+            bon["diagnostics"] = {
+                "pearson_partial_final": round(pr, 4), "kendall_partial_final": round(kd, 4),
+                "first_decision_token": int(warm["trace"]["round_L"][0]),
+                "improvement_score": round(sr.improvement_score(ob["trace"]["final_scores"],
+                                                                 results[-1]["best_score"]), 2),
+                "relative_gpu_compute": round(s_per_prompt / tb, 4)}
         del wsb
         torch.cuda.empty_cache()
 
@@ -229,6 +258,7 @@ def main():
                                + f", prompt {cfg.prompt_len}, "
                                f"N={cfg.n}, tau={cfg.tau}, alpha={cfg.alpha}, {cfg.max_new_tokens} new tokens",
                    "reward": args.reward,
+                   "tau_from": "free device memory" if args.memory_plan else "given",
                    "reward_kv": "recomputed each round" if (args.reward_recompute or kind != sr.SR_REWARD_MODEL)
                                 else "cached across rounds",
                    "N": cfg.n, "alpha": cfg.alpha, "tau": cfg.tau, "max_new_tokens": cfg.max_new_tokens,

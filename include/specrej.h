@@ -191,6 +191,21 @@ typedef struct {
 sr_status sr_workspace_size(const sr_model *gen, const sr_model *rm, int32_t prompt_len,
                             const sr_params *p, size_t *bytes);
 
+/* Memory-driven sizing (Algorithm 1, first step: the initial batch and the
+ * decision token follow from the memory available, as in section 5 where
+ * the system finds how many tokens fit before memory runs out).  Given the
+ * bytes the caller can give the workspace (for instance the device's free
+ * memory after the weights), writes to *out a copy of *p whose
+ *   - tau is the largest in [1, max_new_tokens] with
+ *     sr_workspace_size(out) <= capacity_bytes, when p->n >= 1 (b_init = n
+ *     given, the KV budget n * tau taken from memory); or
+ *   - n is the largest in [1, 4096] with sr_workspace_size(out) <=
+ *     capacity_bytes, when p->n == 0 (tau given, b_init taken from memory).
+ * Every other field is copied.  SR_ERR_WORKSPACE_TOO_SMALL if even tau = 1
+ * (or n = 1) does not fit; other errors as sr_workspace_size.  Host only. */
+sr_status sr_plan_for_memory(const sr_model *gen, const sr_model *rm, int32_t prompt_len,
+                             const sr_params *p, size_t capacity_bytes, sr_params *out);
+
 /* Speculative Rejection (section 4.2, Algorithm 1; Best-of-N when alpha=0).
  *  prompt       HOST int32 [prompt_len], token ids in [0, vocab).
  *  workspace    DEVICE buffer of ws_bytes >= sr_workspace_size(...), 256-byte
@@ -334,6 +349,22 @@ sr_status sr_reward_scores(const sr_model *gen, const sr_model *rm, const int32_
                            int32_t prompt_len, const sr_params *p, const int32_t *tokens,
                            const int32_t *lens, int32_t rows, int32_t max_len, float *scores,
                            void *workspace, size_t ws_bytes, void *stream);
+
+/* Evaluation diagnostics (host arrays, host only, double precision).
+ * Pearson correlation and Kendall's coefficient of n >= 2 finite pairs, as
+ * Appendix B defines them for the partial and final rewards of one
+ * prompt's candidates: Kendall = 2 / (n (n - 1)) * sum over i < j of
+ * sgn(x_i - x_j) sgn(y_i - y_j), tied pairs counting zero (O(n^2) pairs).
+ * *pearson is NaN when either sample is constant.  SR_ERR_INVALID_ARG on
+ * NULL pointers, n < 2 or non-finite values. */
+sr_status sr_correlation(const float *x, const float *y, int32_t n, double *pearson, double *kendall);
+
+/* Improvement score of section 5 (eq. subopt.experiment): the reward of the
+ * Speculative Rejection answer sr_reward placed on the range of the n >= 1
+ * Best-of-N rewards bon_rewards (HOST float [n]):
+ * (1 - (max - sr_reward) / (max - min)) * 100; NaN when max == min.
+ * SR_ERR_INVALID_ARG on NULL pointers, n < 1 or non-finite values. */
+sr_status sr_improvement_score(const float *bon_rewards, int32_t n, float sr_reward, double *score);
 
 #ifdef __cplusplus
 }

@@ -15,6 +15,8 @@ Contents, each citing the passage it follows:
 * ``specrej``     -- Best-of-N (section 3) and Speculative Rejection
                      (section 4.2, Algorithm 1 and eqs. partial-reward-set,
                      cutoff-threshold, accepted-set, output).
+* ``diagnostics`` -- improvement score and relative compute (section 5),
+                     Pearson and Kendall correlation (Appendix B).
 
 Precision: the paper fixes none.  Model arithmetic is float64 on the given
 weights; the sampler's decision (float logits -> integer token) is taken in

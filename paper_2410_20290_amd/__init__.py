@@ -87,6 +87,8 @@ def lib():
         L.sr_keep_count.argtypes = [_i32, _f64]
         L.sr_keep_count.restype = _i32
         L.sr_workspace_size.argtypes = [P(sr_model), P(sr_model), _i32, P(sr_params), P(ctypes.c_size_t)]
+        L.sr_plan_for_memory.argtypes = [P(sr_model), P(sr_model), _i32, P(sr_params), ctypes.c_size_t,
+                                         P(sr_params)]
         L.sr_generate.argtypes = [P(sr_model), P(sr_model), _vp, _i32, P(sr_params), _vp, ctypes.c_size_t,
                                   _vp, _vp, P(sr_result), P(sr_trace)]
         L.sr_philox_fill.argtypes = [_u64, _vp, _i32, _vp, _vp]
@@ -107,7 +109,10 @@ def lib():
         L.sr_decode_attention_scratch.restype = ctypes.c_size_t
         L.sr_prefill_attention.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
                                            _i32, _vp, _vp]
-        for f in ("sr_projection", "sr_decode_attention", "sr_prefill_attention", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
+        L.sr_correlation.argtypes = [_vp, _vp, _i32, P(ctypes.c_double), P(ctypes.c_double)]
+        L.sr_improvement_score.argtypes = [_vp, _i32, _f32, P(ctypes.c_double)]
+        for f in ("sr_projection", "sr_decode_attention", "sr_prefill_attention", "sr_plan_for_memory",
+                  "sr_correlation", "sr_improvement_score", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
                   "sr_logits_teacher_forced", "sr_reward_scores"):
             getattr(L, f).restype = _i32
         _lib = L
@@ -185,6 +190,34 @@ def workspace_size(gen: DeviceModel, rm: DeviceModel, prompt_len: int, p: sr_par
     _check(lib().sr_workspace_size(ctypes.byref(gen.desc), _mref(rm), prompt_len, ctypes.byref(p),
                                    ctypes.byref(out)))
     return int(out.value)
+
+
+def plan_for_memory(gen: DeviceModel, rm: DeviceModel, prompt_len: int, p: sr_params, capacity_bytes: int) -> sr_params:
+    """sr_plan_for_memory: p with the largest tau (p.n >= 1) or n (p.n == 0)
+    whose workspace fits in capacity_bytes."""
+    out = sr_params()
+    _check(lib().sr_plan_for_memory(ctypes.byref(gen.desc), _mref(rm), prompt_len, ctypes.byref(p),
+                                    int(capacity_bytes), ctypes.byref(out)))
+    return out
+
+
+def correlation(x, y):
+    """sr_correlation: (Pearson, Kendall) of the paired host arrays x, y."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    y = np.ascontiguousarray(np.asarray(y, dtype=np.float32))
+    if x.shape != y.shape or x.ndim != 1:
+        raise ValueError("x and y must be 1-D arrays of one length")
+    pr, kd = ctypes.c_double(0.0), ctypes.c_double(0.0)
+    _check(lib().sr_correlation(x.ctypes.data, y.ctypes.data, len(x), ctypes.byref(pr), ctypes.byref(kd)))
+    return pr.value, kd.value
+
+
+def improvement_score(bon_rewards, sr_reward: float) -> float:
+    """sr_improvement_score over the Best-of-N rewards (host array)."""
+    z = np.ascontiguousarray(np.asarray(bon_rewards, dtype=np.float32))
+    out = ctypes.c_double(0.0)
+    _check(lib().sr_improvement_score(z.ctypes.data, len(z), float(sr_reward), ctypes.byref(out)))
+    return out.value
 
 
 def alloc_workspace(nbytes: int, device="cuda"):

@@ -692,13 +692,30 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   for (int t = 0; t < nk; ++t) {
     // step t landed; every wave is done with step t - 1's buffer
     constexpr int VMN = (NST - 2) * D;
-    static_assert(VMN == 0 || VMN == 10 || VMN == 12 || VMN == 16 || VMN == 18 || VMN == 24, "wait count");
+    static_assert(VMN >= 0 && VMN <= 48 && VMN % 2 == 0, "wait count");
     if constexpr (VMN == 0) SR_VMB(0);
+    else if constexpr (VMN == 2) SR_VMB(2);
+    else if constexpr (VMN == 4) SR_VMB(4);
+    else if constexpr (VMN == 6) SR_VMB(6);
+    else if constexpr (VMN == 8) SR_VMB(8);
     else if constexpr (VMN == 10) SR_VMB(10);
     else if constexpr (VMN == 12) SR_VMB(12);
+    else if constexpr (VMN == 14) SR_VMB(14);
     else if constexpr (VMN == 16) SR_VMB(16);
     else if constexpr (VMN == 18) SR_VMB(18);
-    else SR_VMB(24);
+    else if constexpr (VMN == 20) SR_VMB(20);
+    else if constexpr (VMN == 22) SR_VMB(22);
+    else if constexpr (VMN == 24) SR_VMB(24);
+    else if constexpr (VMN == 26) SR_VMB(26);
+    else if constexpr (VMN == 28) SR_VMB(28);
+    else if constexpr (VMN == 30) SR_VMB(30);
+    else if constexpr (VMN == 32) SR_VMB(32);
+    else if constexpr (VMN == 36) SR_VMB(36);
+    else if constexpr (VMN == 40) SR_VMB(40);
+    else if constexpr (VMN == 42) SR_VMB(42);
+    else if constexpr (VMN == 44) SR_VMB(44);
+    else if constexpr (VMN == 48) SR_VMB(48);
+    else static_assert(VMN < 0, "add this wait count");
     issue(min(t + NST - 1, nk - 1), (t + NST - 1) % NST);
     const bf16_t* base = lds + (t % NST) * STAGE;
     bf16x8 a0[TI], b0[NB][TJ], a1[TI], b1[NB][TJ];

@@ -979,6 +979,8 @@ static sr_status guard(F&& f) {
   }
 }
 
+void set_last_error(const char* msg) { t_err = msg; }
+
 }  // namespace sr
 
 using namespace sr;
@@ -1006,6 +1008,36 @@ sr_status sr_workspace_size(const sr_model* gen, const sr_model* rm, int32_t pro
     size_t tot = 0;
     carve(nullptr, gd, rd, pl, &tot);
     *bytes = tot;
+  });
+}
+
+sr_status sr_plan_for_memory(const sr_model* gen, const sr_model* rm, int32_t prompt_len, const sr_params* p,
+                             size_t capacity_bytes, sr_params* out) {
+  return guard([&] {
+    SR_REQUIRE(p != nullptr && out != nullptr, SR_ERR_INVALID_ARG, "params is NULL");
+    const bool pick_n = p->n == 0;
+    sr_params q = *p;
+    if (pick_n) q.n = 1;
+    // the largest value of the free field whose workspace fits; the size
+    // never decreases as n or tau grows, so a bisection finds it
+    auto fits = [&](int v) {
+      sr_params t = q;
+      (pick_n ? t.n : t.tau) = v;
+      size_t need = 0;
+      const sr_status st = sr_workspace_size(gen, rm, prompt_len, &t, &need);
+      SR_REQUIRE(st == SR_OK, st, t_err);
+      return need <= capacity_bytes;
+    };
+    int lo = 1, hi = pick_n ? kMaxN : std::max(1, p->max_new_tokens);
+    SR_REQUIRE(fits(lo), SR_ERR_WORKSPACE_TOO_SMALL,
+               std::string("capacity below the workspace of ") + (pick_n ? "n = 1" : "tau = 1"));
+    while (lo < hi) {
+      const int mid = lo + (hi - lo + 1) / 2;
+      if (fits(mid)) lo = mid;
+      else hi = mid - 1;
+    }
+    (pick_n ? q.n : q.tau) = lo;
+    *out = q;
   });
 }
 

@@ -5,7 +5,8 @@
         then the decode projections of the 8B-shaped generator at 103 and at
         21 rows, three launches each; prints the algorithmic bytes of each.
     python3 <repo>/paper_2410_20290_amd/probes.py gemm [rows,rows,...]
-        Graph-replay timing of the projections at the given row counts.
+        Graph-replay timing of the projections at the given row counts, each
+        launch on a different copy of the weights (>= 1 GiB in all).
     python3 <repo>/paper_2410_20290_amd/probes.py sample
         Timing of the sampler over 512, 103 and 21 rows of 8B-shaped logits.
     python3 <repo>/paper_2410_20290_amd/probes.py attn
@@ -90,7 +91,19 @@ def gemm(rows):
             if name == "head" and M > 512:
                 continue
             x, w, out, part, need, nw = _operands(torch, M, N, K, mode)
-            t = gtime(lambda: _launch(torch, x, w, out, part, need, M, N, K, mode))
+            # weight copies totalling >= 1 GiB, one per launch in turn, so that
+            # no launch finds its weights in the last-level cache (as in a
+            # decode step, which streams every layer's weights once)
+            copies = [w] + [w.clone() for _ in range(max(0, -(-(1 << 30) // (2 * nw * K)) - 1))]
+            turn = [0]
+
+            def one():
+                wc = copies[turn[0] % len(copies)]
+                turn[0] += 1
+                _launch(torch, x, wc, out, part, need, M, N, K, mode)
+
+            t = gtime(lambda: [one() for _ in range(len(copies))]) / len(copies)
+            del copies
             fl = 2.0 * M * nw * K
             by = 2.0 * (nw * K + M * K) + M * N * 4
             print(json.dumps({"M": M, "op": name, "us": round(t * 1e6, 1), "TFLOPs": round(fl / t / 1e12, 1),

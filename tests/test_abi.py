@@ -30,7 +30,7 @@ def declared_symbols():
 
 def test_header_symbols_exported(L):
     names = declared_symbols()
-    assert len(names) == 15, names
+    assert len(names) == 18, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -94,6 +94,53 @@ def test_reward_cache_size():
                                                                  reward_kind=sr.SR_REWARD_LOGPROB,
                                                                  reward_recompute=rc))[1] for rc in (0, 1)]
     assert b[0] == b[1]
+
+
+def plan(L, gen, rm, P, p, cap):
+    out = sr.sr_params()
+    st = L.sr_plan_for_memory(ctypes.byref(gen), ctypes.byref(rm), P, ctypes.byref(p), cap, ctypes.byref(out))
+    return st, out
+
+
+@pytest.mark.parametrize("name,alpha", [("tiny_fp32", 0.5), ("small_bf16", 0.75), ("8b_bf16", 0.8),
+                                        ("8b_bf16", 0.0), ("8b_bf16_n1024", 0.5)])
+def test_plan_for_memory_is_maximal(L, name, alpha):
+    """Algorithm 1's memory-driven sizing: the chosen tau (n given) or n (tau
+    given) is the largest whose workspace fits the capacity."""
+    c = synth.CONFIGS[name]
+    gen, rm = fake_model(c.model, False), fake_model(c.model, True)
+    p = sr.make_params(c.n, alpha, c.tau, c.max_new_tokens)
+    base = ws_size(L, gen, rm, c.prompt_len, p)[1]
+    for cap in (base, base + 1, base * 3 // 2, base * 4, 288 * 10**9):
+        st, out = plan(L, gen, rm, c.prompt_len, p, cap)
+        assert st == sr.SR_OK, sr.last_error()
+        assert out.n == c.n and out.alpha == alpha and out.max_new_tokens == c.max_new_tokens
+        fit = lambda tau: ws_size(L, gen, rm, c.prompt_len, sr.make_params(c.n, alpha, tau, c.max_new_tokens))[1]
+        assert fit(out.tau) <= cap
+        assert out.tau == c.max_new_tokens or fit(out.tau + 1) > cap
+        if cap == base:
+            assert out.tau >= c.tau
+    # n from memory at the given tau
+    q = sr.make_params(0, alpha, c.tau, c.max_new_tokens)
+    for cap in (base, base * 2, 288 * 10**9):
+        st, out = plan(L, gen, rm, c.prompt_len, q, cap)
+        assert st == sr.SR_OK, sr.last_error()
+        fitn = lambda n: ws_size(L, gen, rm, c.prompt_len, sr.make_params(n, alpha, c.tau, c.max_new_tokens))[1]
+        assert out.tau == c.tau and fitn(out.n) <= cap and (out.n == 4096 or fitn(out.n + 1) > cap)
+        if cap == base:
+            assert out.n >= c.n
+    # too little memory for anything
+    st, _ = plan(L, gen, rm, c.prompt_len, p, 1 << 20)
+    assert st == sr.SR_ERR_WORKSPACE_TOO_SMALL and sr.last_error()
+
+
+def test_plan_for_memory_rejects_bad_input(L):
+    c = synth.CONFIGS["tiny_fp32"]
+    gen, rm = fake_model(c.model, False), fake_model(c.model, True)
+    assert plan(L, gen, rm, 32, sr.make_params(16, 1.5, 16, 64), 1 << 40)[0] == sr.SR_ERR_INVALID_ARG
+    assert plan(L, gen, rm, 0, sr.make_params(16, 0.5, 16, 64), 1 << 40)[0] == sr.SR_ERR_INVALID_ARG
+    assert L.sr_plan_for_memory(ctypes.byref(gen), ctypes.byref(rm), 32, None, 1 << 40, None) == \
+        sr.SR_ERR_INVALID_ARG
 
 
 BAD_PARAMS = [

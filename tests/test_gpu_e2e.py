@@ -112,6 +112,56 @@ def test_reward_cache_matches_recompute(name, over, rtol):
             assert abs(fb[a["best_index"]] - fb[b["best_index"]]) <= 2 * rtol * np.abs(fb[m]).max()
 
 
+def test_diagnostics_against_best_of_n():
+    """Section 5 / Appendix B diagnostics of a run: Speculative Rejection's
+    candidates are prefixes of Best-of-N's at the same seed, so Best-of-N's
+    final rewards are the final rewards of the candidates whose partial
+    rewards the first cut ranked; the answer's reward is Best-of-N's reward of
+    the same candidate, so the improvement score is at most 100."""
+    torch, sr = need_gpu()
+    say("small_bf16 diagnostics vs best-of-N")
+    c, _, a = gpu_run("small_bf16")
+    _, _, b = gpu_run("small_bf16", alpha=0.0)
+    ta, tb = a["trace"], b["trace"]
+    for k in range(c.n):
+        la = ta["all_len"][k]
+        assert ta["all_tokens"][k, :la].tolist() == tb["all_tokens"][k, :la].tolist(), k
+    L0, b0, K0, cand0, partial, _ = trace_rounds(a)[0]
+    assert b0 == c.n and cand0 == list(range(c.n))
+    final = tb["final_scores"]
+    assert not np.isnan(final).any()
+    pr, kd = sr.correlation(partial, final)
+    from oracle import diagnostics as dg
+    assert abs(pr - dg.pearson(partial, final)) < 1e-9 and abs(kd - dg.kendall(partial, final)) < 1e-12
+    assert -1.0 <= pr <= 1.0 and -1.0 <= kd <= 1.0
+    best = a["best_index"]
+    assert abs(a["best_score"] - final[best]) <= tol(c) * np.abs(final).max()
+    score = sr.improvement_score(final, a["best_score"])
+    assert score <= 100.0 + 100.0 * tol(c) * np.abs(final).max() / (final.max() - final.min())
+
+
+def test_memory_planned_run_matches_given_budget():
+    """Algorithm 1's memory-driven sizing on the device: with exactly the
+    workspace of tau = 16 available, the planner picks tau = 16 and the run is
+    the one with that budget given; with the device's free memory it picks the
+    largest tau that fits, and the run completes within that workspace."""
+    torch, sr = need_gpu()
+    say("memory-planned tiny_fp32 run")
+    c, gen, rm, prompt = device_models("tiny_fp32")
+    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed)
+    need = sr.workspace_size(gen, rm, len(prompt), p)
+    q = sr.plan_for_memory(gen, rm, len(prompt), p, need)
+    assert (q.n, q.tau) == (c.n, c.tau)
+    a = sr.generate(gen, rm, prompt, p)
+    b = sr.generate(gen, rm, prompt, q)
+    assert a["tokens"] == b["tokens"] and a["best_index"] == b["best_index"] and a["rounds"] == b["rounds"]
+    free, _ = torch.cuda.mem_get_info()
+    big = sr.plan_for_memory(gen, rm, len(prompt), p, free // 2)
+    assert big.tau == c.max_new_tokens          # a tiny model fits every budget: one round, as Best-of-N
+    o = sr.generate(gen, rm, prompt, big)
+    assert o["rounds"] == 0 and o["generated_tokens"] == c.n * c.max_new_tokens
+
+
 @pytest.mark.parametrize("name", ["small_bf16"])
 def test_bf16_audit(name):
     torch, sr = need_gpu()
