@@ -358,9 +358,13 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // registers); each instruction moves 8 rows of 128 bytes, so every request
 // to L2 is a whole 128-byte line.  A K step is four quarter steps of 16
 // MFMAs per wave (4 waves, each a 128 x 128 tile of 4 x 4
-// v_mfma_f32_32x32x16_bf16 accumulators); the fragment reads of the next
-// quarter and the DMAs of the step after next run between the MFMAs, and the
-// one barrier per step sits before the last quarter.  LDS rows hold eight
+// v_mfma_f32_32x32x16_bf16 accumulators).  The fragments of quarters 1-3
+// are read under the MFMAs of quarters 0 and 1 (three register sets that
+// rotate from step to step), so the buffer is free after quarter 1: the
+// DMAs of the step after next are spread over quarters 2 and 3 (A rows, then
+// B rows), which keeps the vector-memory path from backing up into the MFMA
+// issue.  Two barriers per step: after quarter 1 (buffer read by all waves)
+// and after quarter 2 (next step landed in all waves).  LDS rows hold eight
 // 16-byte chunks; chunk c of tile row r sits in slot c ^ (r & 7) ^ ((r >> 3) & 3)
 // (a function of r mod 32, so fragment blocks of 32 rows share it), which puts the fragment reads of any 8 or 16 consecutive rows on distinct
 // banks.
@@ -408,15 +412,14 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   }
   const char* Ab = reinterpret_cast<const char*>(A + k_begin);
   const char* Bb = reinterpret_cast<const char*>(B + k_begin);
-  auto issue = [&](int st, int buf) {
-    bf16_t* sa = lds + buf * STAGE;
-    bf16_t* sb = sa + BM * BK;
-    const int kb = st * BK * 2;
+  // half h of stage `st` into buffer `buf`: the A rows (h = 0) or the B rows
+  // (h = 1), 8 instructions per wave
+  auto issue_half = [&](int st, int buf, int h) {
+    bf16_t* dst = lds + buf * STAGE + h * BM * BK;
+    const char* src = (h ? Bb : Ab) + st * BK * 2;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_global_load_lds(Ab + kb + aoff[i], sa + (wave + 4 * i) * 512, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(Bb + kb + boff[i], sb + (wave + 4 * i) * 512, 16, 0, 0);
-    }
+    for (int i = 0; i < 8; ++i)
+      __builtin_amdgcn_global_load_lds(src + (h ? boff[i] : aoff[i]), dst + (wave + 4 * i) * 512, 16, 0, 0);
   };
 
   // Fragment reads: lane l holds row l % 32 of a 32-row block, K chunk
@@ -448,8 +451,17 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
   };
-  // a quarter whose eight fragment reads follow its first eight MFMAs
-  auto reads_under_mfma = [] {
+  // instruction interleavings: (MFMA, fragment read) x 16; (MFMA, read) x 8
+  // then 8 MFMAs; (2 MFMAs, DMA) x 8; (MFMA, read, MFMA, DMA) x 8
+  auto reads16 = [] {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto reads8 = [] {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -458,45 +470,68 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
-
-  // Every step issues the DMAs of the step after next; past the last step
-  // the source is clamped to the last step (data never read), which keeps
-  // every wait below the same at each step.
-  issue(0, 0);
-  issue(min(1, nk - 1), 1);
-  SR_VM_BARRIER(16);
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
-  bf16x8 a0[4], b0[4], a1[4], b1[4];
-  read_frags(0, 0, a0, b0);
-  for (int t = 0; t < nk; ++t) {
-    const int buf = t & 1;
-    read_frags(buf, 1, a1, b1);
-    mfma(a0, b0);
-    reads_under_mfma();
-    read_frags(buf, 2, a0, b0);
-    mfma(a1, b1);
-    reads_under_mfma();
-    read_frags(buf, 3, a1, b1);
-    mfma(a0, b0);
-    reads_under_mfma();
-    // step t + 1 landed; every wave is done reading buffer `buf`
-    SR_VM_BARRIER(0);
+  auto dma8 = [] {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
-    // (after the last step this reads a stale buffer that is never used)
-    read_frags(buf ^ 1, 0, a0, b0);
-    issue(min(t + 2, nk - 1), buf);
-    mfma(a1, b1);
+  };
+  auto reads8_dma8 = [] {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x010, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Every step issues the DMAs of the step after next; past the last step
+  // the source is clamped to the last step (data never read), which keeps
+  // every wait below the same at each step.
+  issue_half(0, 0, 0);
+  issue_half(0, 0, 1);
+  issue_half(min(1, nk - 1), 1, 0);
+  issue_half(min(1, nk - 1), 1, 1);
+  SR_VM_BARRIER(16);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
+  bf16x8 a0[4], b0[4], a1[4], b1[4], a2[4], b2[4];
+  read_frags(0, 0, a0, b0);
+  // One K step with its quarter 0 in (xa, xb); quarter 3 reuses those
+  // registers and the next step's quarter 0 goes to (ya, yb).
+  auto step = [&](int t, bf16x8(&xa)[4], bf16x8(&xb)[4], bf16x8(&ya)[4], bf16x8(&yb)[4], bf16x8(&za)[4],
+                  bf16x8(&zb)[4]) {
+    const int buf = t & 1;
+    const int nx = min(t + 2, nk - 1);
+    read_frags(buf, 1, ya, yb);
+    read_frags(buf, 2, za, zb);
+    mfma(xa, xb);
+    reads16();
+    read_frags(buf, 3, xa, xb);
+    mfma(ya, yb);
+    reads8();
+    // every wave has read all of buffer `buf`
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+    issue_half(nx, buf, 0);
+    mfma(za, zb);
+    dma8();
+    // step t + 1 landed: all but this wave's 8 newest DMAs, in every wave
+    SR_VM_BARRIER(8);
+    __builtin_amdgcn_sched_barrier(0);
+    // (after the last step this reads a stale buffer that is never used)
+    read_frags(buf ^ 1, 0, ya, yb);
+    issue_half(nx, buf, 1);
+    mfma(xa, xb);
+    reads8_dma8();
+  };
+  for (int t = 0; t < nk; t += 3) {
+    step(t, a0, b0, a1, b1, a2, b2);
+    if (t + 1 < nk) step(t + 1, a1, b1, a2, b2, a0, b0);
+    if (t + 2 < nk) step(t + 2, a2, b2, a0, b0, a1, b1);
   }
   // no DMA may still be writing LDS when the work-group ends
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
