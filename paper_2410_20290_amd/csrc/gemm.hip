@@ -599,6 +599,193 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 #undef SR_VM_BARRIER
 
 
+// ------------------------- bf16 MFMA GEMM, a few hundred rows (LDS DMA)
+// 256 x 128 block tile (PAIRED: gate and up rows interleaved in groups of
+// 32, 64 output columns), K step 64, three LDS stages of 48 KB.  With a
+// third stage the buffer refilled during step t (that of step t - 1) is
+// free from its start, so the 12 DMA instructions per wave of the step after
+// next are spread over quarter steps 0-2 and the data of step t + 1 has a
+// whole step to land; one barrier per step, before quarter 3.  4 waves, each
+// a 128 x 64 tile of 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators; LDS rows
+// and their swizzle as in the 256 x 256 kernel.
+#define SR_VMB3(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
+
+template <bool PAIRED>
+__global__ void __launch_bounds__(256)
+gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
+                 int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                 float* __restrict__ partial) {
+  constexpr int BM = 256, BNL = 128, BK = 64, NST = 3;
+  constexpr int BN_OUT = PAIRED ? 64 : 128;
+  constexpr int STAGE = (BM + BNL) * BK;      // bf16 elements per stage
+  constexpr int DA = BM / 32, DB = BNL / 32;  // DMA instructions per wave per stage
+  static_assert(DA + DB == 12, "the wait count below assumes 12 DMAs per wave per stage");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
+
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN_OUT - 1) / BN_OUT, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave >> 1) * 128, wn0 = (wave & 1) * 64;
+  const int m0 = tile.m * BM, n0 = tile.n * BN_OUT;
+  const int k_begin = tile.split * k_per_split;
+  const int nk = k_per_split / BK;
+
+  // DMA sources: instruction i of a wave moves tile rows 8 (w + 4 i) .. + 7
+  // (A rows for i < DA, then B rows); lane l writes slot l % 8 of row l / 8.
+  uint32_t aoff[DA], boff[DB];
+#pragma unroll
+  for (int i = 0; i < DA; ++i) {
+    const int r = 8 * (wave + 4 * i) + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 3);
+    aoff[i] = (uint32_t)(((int64_t)min(m0 + r, M - 1) * lda + c * 8) * 2);
+  }
+#pragma unroll
+  for (int i = 0; i < DB; ++i) {
+    const int r = 8 * (wave + 4 * i) + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7) ^ ((r >> 3) & 3);
+    int n;
+    int64_t off = 0;
+    if (PAIRED) {
+      const int grp = r >> 5;
+      n = n0 + (grp >> 1) * 32 + (r & 31);
+      off = (grp & 1) * pair_off;
+    } else {
+      n = n0 + r;
+    }
+    boff[i] = (uint32_t)((off + (int64_t)min(n, N - 1) * ldb + c * 8) * 2);
+  }
+  const char* Ab = reinterpret_cast<const char*>(A + k_begin);
+  const char* Bb = reinterpret_cast<const char*>(B + k_begin);
+  auto dma = [&](int st, int buf, int i) {
+    bf16_t* sa = lds + buf * STAGE;
+    const int kb = st * BK * 2;
+    if (i < DA) __builtin_amdgcn_global_load_lds(Ab + kb + aoff[i], sa + (wave + 4 * i) * 512, 16, 0, 0);
+    else __builtin_amdgcn_global_load_lds(Bb + kb + boff[i - DA], sa + BM * BK + (wave + 4 * (i - DA)) * 512, 16, 0, 0);
+  };
+
+  const int fr = lane & 31, fg = lane >> 5;
+  const int sw = (fr & 7) ^ ((fr >> 3) & 3);
+  int foff[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) foff[q] = fr * BK + 8 * ((2 * q + fg) ^ sw);
+  auto read_frags = [&](int buf, int q, bf16x8(&af)[4], bf16x8(&bfr)[2]) {
+    const bf16_t* sa = lds + buf * STAGE + foff[q];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(sa + (wm0 + 32 * i) * BK);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(sa + (BM + wn0 + 32 * j) * BK);
+  };
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  auto mfma = [&](const bf16x8(&af)[4], const bf16x8(&bfr)[2]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+  };
+  // quarters 0-2: (MFMA, read, MFMA, DMA) x 4, then the last two reads
+  auto reads_dmas = [] {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // quarter 3: (MFMA, read) x 6, then 2 MFMAs
+  auto reads = [] {
+#pragma unroll
+    for (int q = 0; q < 6; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Every step issues the DMAs of the step after next (clamped to the last
+  // step past the end: data never read), so every wait is the same.
+#pragma unroll
+  for (int i = 0; i < DA + DB; ++i) dma(0, 0, i);
+#pragma unroll
+  for (int i = 0; i < DA + DB; ++i) dma(min(1, nk - 1), 1, i);
+  SR_VMB3(12);  // step 0 landed
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
+  bf16x8 a0[4], b0[2], a1[4], b1[2];
+  read_frags(0, 0, a0, b0);
+  for (int t = 0; t < nk; ++t) {
+    const int buf = t % 3, nb = (t + 1) % 3, wb = (t + 2) % 3;
+    const int nx = min(t + 2, nk - 1);
+    read_frags(buf, 1, a1, b1);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma(nx, wb, i);
+    mfma(a0, b0);
+    reads_dmas();
+    read_frags(buf, 2, a0, b0);
+#pragma unroll
+    for (int i = 4; i < 8; ++i) dma(nx, wb, i);
+    mfma(a1, b1);
+    reads_dmas();
+    read_frags(buf, 3, a1, b1);
+#pragma unroll
+    for (int i = 8; i < 12; ++i) dma(nx, wb, i);
+    mfma(a0, b0);
+    reads_dmas();
+    // step t + 1 landed (all but this wave's 12 newest DMAs) in every wave,
+    // and every wave has read all it needs of buffer `buf`
+    SR_VMB3(12);
+    __builtin_amdgcn_sched_barrier(0);
+    // (after the last step this reads a stale buffer that is never used)
+    read_frags(nb, 0, a0, b0);
+    mfma(a1, b1);
+    reads();
+  }
+  // no DMA may still be writing LDS when the work-group ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
+      if (m >= M) continue;
+      if (PAIRED) {
+        const int n = n0 + (wn0 >> 1) + fr;
+        if (n >= N) continue;
+        const float g = acc[i][0][e], u = acc[i][1][e];
+        if (partial) {
+          float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
+          p[n] = g;
+          p[N + n] = u;
+        } else {
+          store_out(epi, m, n, silu(g) * u);
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = n0 + wn0 + j * 32 + fr;
+          if (n >= N) continue;
+          if (partial)
+            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
+          else
+            epi_one(epi, m, n, acc[i][j][e]);
+        }
+      }
+    }
+}
+#undef SR_VMB3
+
 // ------------------------------------- bf16 MFMA GEMM, few rows (LDS DMA)
 // For the decode projections (a few hundred rows at most) the weights are
 // streamed once from HBM; what matters is keeping enough of them in flight
@@ -1070,6 +1257,16 @@ static int stream_max_rows() {
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
 
+// Rows up to which the three-stage 256 x 128 tile is used (above the
+// streaming kernel's rows).
+static int dma3_max_rows() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_DMA3_MAX_M");
+    return e ? atoi(e) : 512;
+  }();
+  return v;
+}
+
 // Rows below which the 128 x 128 streaming tile (K step 64) takes over from
 // the other tiles for unpaired projections with at most 65536 outputs per
 // row; off by default (it measured even with them end to end).
@@ -1087,6 +1284,7 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.big = false;
   p.skinny = false;
   p.dma = false;
+  p.dma3 = false;
   p.stream = 0;
   p.stream_bn = 0;
   p.stream_bk = 128;
@@ -1099,6 +1297,17 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     const int64_t tiles = (int64_t)((M + p.stream - 1) / p.stream) * ((N + p.stream_bn - 1) / p.stream_bn);
     int splits = 1;
     while (tiles * splits * 2 <= 256 && K % (splits * 2 * 128) == 0) splits *= 2;
+    p.splits = splits;
+    return p;
+  }
+  if (M > stream_max_rows() && M <= dma3_max_rows() && K % 64 == 0) {
+    // A few hundred rows (the first decode round): 256 x 128 tiles with
+    // three stages; split K (each split a multiple of 64 and at least 512
+    // long) by powers of two while the grid stays within 256.
+    p.dma3 = true;
+    const int64_t tiles = (int64_t)((M + 255) / 256) * ((N + (paired ? 63 : 127)) / (paired ? 64 : 128));
+    int splits = 1;
+    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 64) == 0 && K / (splits * 2) >= 512) splits *= 2;
     p.splits = splits;
     return p;
   }
@@ -1259,6 +1468,16 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
       else SR_STREAM(128, 64, 2, 2, 3, false);
     }
 #undef SR_STREAM
+    SR_CHECK_LAUNCH();
+  } else if (plan.dma3 && dma_offsets_fit(g)) {
+    const int bn_out = g.paired ? 64 : 128;
+    dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
+    if (g.paired)
+      hipLaunchKernelGGL(gemm_dma3_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+    else
+      hipLaunchKernelGGL(gemm_dma3_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     SR_CHECK_LAUNCH();
   } else if (plan.dma && dma_offsets_fit(g)) {
     const int bn_out = g.paired ? 128 : 256;
