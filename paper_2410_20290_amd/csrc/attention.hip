@@ -203,7 +203,7 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
       }
     }
     const int qh = h * G + g;
-    if (splits == 1) {
+    if (out) {
       out[((int64_t)row * hq + qh) * HD + dd] = from_f32<T>(A / L);
     } else {
       float* p = part + (((int64_t)row * hq + qh) * splits + split0 + split) * (HD + 2);
@@ -358,7 +358,7 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int dim = 32 * wave + 16 * dt + 4 * fg + e;
-        if (splits == 1) {
+        if (out) {
           out[((int64_t)row * hq + qh) * HD + dim] = f32_to_bf16(o[dt][e] / l);
         } else {
           float* pp = part + (((int64_t)row * hq + qh) * splits + split0 + split) * (HD + 2);
@@ -459,53 +459,54 @@ static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsp
 template <typename T, int HD, int G>
 static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
+  // The batched MFMA pass over the shared prefix (16 rows per work-group)
+  // runs last: the tails leave partial slots and it folds them into its own
+  // result, so no merge pass is needed.
+  auto prefix_pass = [&](int tsplits) {
+    hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
+                       a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows, 0, 0, a.hq,
+                       a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
+    SR_CHECK_LAUNCH();
+  };
   if (tail_by_mfma(a.dtype, HD, G, a.rows)) {
-    // optional batched MFMA pass over the shared prefix (slots 0..psplits-1),
-    // then the streaming kernel over the remaining keys, then the merge
+    // the streaming kernel over the keys past the prefix pass's, then the
+    // prefix pass or (several splits without it) the merge
     const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
-    const int psplits = pre ? (a.P + 63) / 64 : 0;
     const int key0 = pre ? a.P : 0;
     const int keys = a.P + a.lt - key0;
     const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
     const int tsplits = (keys + kps - 1) / kps;
-    const int splits = tsplits + psplits;
-    if (splits > 1)
-      SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
-    if (pre) {
-      hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits),
-                         dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr,
-                         nullptr, a.rows, 0, 0, a.hq, a.hkv, nullptr, qscale, a.part, splits);
-      SR_CHECK_LAUNCH();
+    const bool direct = !pre && tsplits == 1;
+    if (!direct)
+      SR_REQUIRE((size_t)a.rows * a.hq * std::max(tsplits, 1) * (HD + 2) <= a.part_cap, 5,
+                 "attention partial buffer too small");
+    if (tsplits > 0) {
+      DecodeAttnArgs b = a;
+      if (!direct) b.out = nullptr;
+      launch_tail_mfma<G>(b, key0, kps, tsplits, tsplits, 0, qscale, s);
     }
-    if (tsplits > 0) launch_tail_mfma<G>(a, key0, kps, tsplits, splits, psplits, qscale, s);
-    if (splits > 1) {
-      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, splits, a.hq,
+    if (pre) {
+      prefix_pass(tsplits);
+    } else if (!direct) {
+      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, tsplits, a.hq,
                          (T*)a.out);
       SR_CHECK_LAUNCH();
     }
     return;
   }
   if (prefix_by_mfma(a.dtype, HD, a.P, a.rows)) {
-    // prefix partials (slots 0..psplits-1, 64 keys each, 16 rows per
-    // work-group), then the tail partials
-    const int psplits = (a.P + 63) / 64;
+    // tail partials, then the prefix pass
     const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;
     const int tsplits = (a.lt + tkps - 1) / tkps;
-    const int splits = tsplits + psplits;
-    SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5, "attention partial buffer too small");
-    hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, psplits), dim3(64 * G),
-                       0, s, a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows,
-                       0, 0, a.hq, a.hkv, nullptr, qscale, a.part, splits);
-    SR_CHECK_LAUNCH();
+    SR_REQUIRE((size_t)a.rows * a.hq * std::max(tsplits, 1) * (HD + 2) <= a.part_cap, 5,
+               "attention partial buffer too small");
     if (tsplits > 0) {
       hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
                          (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail, (const T*)a.vtail, a.cap,
-                         a.lt, a.hq, a.hkv, tkps, splits, a.part, (T*)a.out, qscale, a.P, psplits);
+                         a.lt, a.hq, a.hkv, tkps, tsplits, a.part, (T*)nullptr, qscale, a.P, 0);
       SR_CHECK_LAUNCH();
     }
-    hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, splits, a.hq,
-                       (T*)a.out);
-    SR_CHECK_LAUNCH();
+    prefix_pass(tsplits);
     return;
   }
   const int keys = a.P + a.lt;
@@ -516,8 +517,8 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
                "attention partial buffer too small");
   hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(splits, a.hkv, a.rows), dim3(256), 0, s,
                      a.q, (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail,
-                     (const T*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (T*)a.out,
-                     qscale, 0, 0);
+                     (const T*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part,
+                     splits == 1 ? (T*)a.out : (T*)nullptr, qscale, 0, 0);
   SR_CHECK_LAUNCH();
   if (splits > 1) {
     hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part,
@@ -661,8 +662,12 @@ constexpr int PF_VROW = 32 + 4;      // V^T tile row (bf16), padded
 
 // PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
 // The 16 "queries" of a work-group are 16 decode rows (lr = rows, one
-// sequence), every prefix key is visible, and the unnormalised output with
-// its running max and sum is written as split 0 of the decode partials.
+// sequence) and every prefix key is visible.  The tails were attended first
+// and left part_splits partial slots per (row, query head) in `part`
+// (unnormalised output, running max, sum); the work-group folds them into
+// its own result by log-sum-exp and writes the attention output.
+// Both forms fetch the next 32-key tile into registers while the current
+// one is computed.
 template <int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
@@ -672,7 +677,6 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   constexpr int HD = 128, NT = 64 * G;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * PF_VROW];
-  // PREFIX_ONLY: blockIdx.z is the prefix split (keys [64 z, 64 z + 64)).
   const int qb = blockIdx.x, h = blockIdx.y, row = PREFIX_ONLY ? 0 : blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fg = lane >> 4;
@@ -696,26 +700,38 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
   const int tlast = min(lr, (qb + 1) * 16) - 1;
-  const int kbeg = PREFIX_ONLY ? blockIdx.z * 64 : 0;
-  const int nkeys = PREFIX_ONLY ? min(P, kbeg + 64) : P + t0 + tlast + 1;
+  const int nkeys = PREFIX_ONLY ? P : P + t0 + tlast + 1;
   const bf16_t* kp = kpre + (int64_t)h * P * HD;
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
   const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * cap * HD;
   const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * cap * HD;
-  for (int kb = kbeg; kb < nkeys; kb += PF_KT) {
-    // stage K [key][dim] and V^T [dim][key]: 32 keys x 16 chunks of 8 dims
-    for (int c = threadIdx.x; c < PF_KT * 16; c += NT) {
-      const int j = c >> 4, cc = c & 15;
-      const int key = kb + j;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (key < nkeys) {
+  // a tile is 32 keys x 16 chunks of 8 dims; thread chunks c = tid + NT i
+  constexpr int CPT = (PF_KT * 16 + NT - 1) / NT;
+  uint4 kreg[CPT], vreg[CPT];
+  auto fetch = [&](int kb) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + NT * i;
+      const int key = kb + (c >> 4), cc = c & 15;
+      kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
+      if (c < PF_KT * 16 && key < nkeys) {
         const bf16_t* kr = key < P ? kp + (int64_t)key * HD : ko + (int64_t)(key - P) * HD;
         const bf16_t* vr = key < P ? vp + (int64_t)key * HD : vo + (int64_t)(key - P) * HD;
-        kv = *reinterpret_cast<const uint4*>(kr + cc * 8);
-        vv = *reinterpret_cast<const uint4*>(vr + cc * 8);
+        kreg[i] = *reinterpret_cast<const uint4*>(kr + cc * 8);
+        vreg[i] = *reinterpret_cast<const uint4*>(vr + cc * 8);
       }
-      *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kv;
-      const uint32_t w4[4] = {vv.x, vv.y, vv.z, vv.w};
+    }
+  };
+  fetch(0);
+  for (int kb = 0; kb < nkeys; kb += PF_KT) {
+    // stage K [key][dim] and V^T [dim][key], then fetch the next tile
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + NT * i;
+      if (c >= PF_KT * 16) break;
+      const int j = c >> 4, cc = c & 15;
+      *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
+      const uint32_t w4[4] = {vreg[i].x, vreg[i].y, vreg[i].z, vreg[i].w};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         Vt[(cc * 8 + 2 * e) * PF_VROW + j] = (bf16_t)(w4[e] & 0xFFFFu);
@@ -723,6 +739,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       }
     }
     __syncthreads();
+    if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
     // S^T for key tiles 0 (keys kb..kb+15) and 1 (kb+16..kb+31)
     f32x4 st[2];
 #pragma unroll
@@ -778,15 +795,30 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   }
   if (qvalid) {
     if (PREFIX_ONLY) {
-      float* pr = part + (((int64_t)t * hq + qh) * part_splits + blockIdx.z) * (HD + 2);
+      // fold in the tail partials of (row t, head qh): slot s holds the
+      // unnormalised output, its maximum and its sum
+      const float* pr = part + ((int64_t)t * hq + qh) * part_splits * (HD + 2);
+      float mx = m;
+      for (int sp = 0; sp < part_splits; ++sp) mx = fmaxf(mx, pr[sp * (HD + 2) + HD]);
+      const float c0 = exp2_or_zero(m - mx);
+      float L = l * c0;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) o[dt] *= c0;
+      for (int sp = 0; sp < part_splits; ++sp) {
+        const float* ps = pr + sp * (HD + 2);
+        const float cs = exp2_or_zero(ps[HD] - mx);
+        L += ps[HD + 1] * cs;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o[dt][i] += ps[dt * 16 + 4 * fg + i] * cs;
+      }
+      const float inv = 1.0f / L;
+      bf16_t* orow = out + ((int64_t)t * hq + qh) * HD;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pr[dt * 16 + 4 * fg + i] = o[dt][i];
-      if (fg == 0) {
-        pr[HD] = m;
-        pr[HD + 1] = l;
-      }
+        for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
     } else {
       const float inv = 1.0f / l;
       bf16_t* orow = out + (((int64_t)row * lr + t) * hq + qh) * HD;

@@ -31,6 +31,10 @@ CASES = [
     ("bf16", 128, 32, 8, 40, 256, 1, 128),
     ("bf16", 128, 32, 8, 128, 256, 50, 64),
     ("bf16", 128, 32, 8, 160, 256, 20, 32),
+    ("bf16", 128, 32, 8, 512, 256, 127, 128),     # first round of the 8B schedule
+    ("bf16", 128, 32, 8, 512, 256, 1, 128),
+    ("bf16", 128, 64, 8, 300, 256, 0, 16),
+    ("bf16", 128, 16, 8, 129, 40, 300, 320),
     ("bf16", 128, 64, 8, 12, 100, 90, 96),
     ("bf16", 128, 32, 8, 17, 0, 77, 80),
     ("bf16", 128, 32, 8, 5, 256, 0, 16),
