@@ -666,8 +666,9 @@ constexpr int PF_VROW = 32 + 4;      // V^T tile row (bf16), padded
 // and left part_splits partial slots per (row, query head) in `part`
 // (unnormalised output, running max, sum); the work-group folds them into
 // its own result by log-sum-exp and writes the attention output.
-// Both forms fetch the next 32-key tile into registers while the current
-// one is computed.
+// The prefix form fetches the next 32-key tile into registers while the
+// current one is computed (the prefill form, with many work-groups per CU,
+// fetches each tile just before staging it).
 template <int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
@@ -722,9 +723,10 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       }
     }
   };
-  fetch(0);
+  if constexpr (PREFIX_ONLY) fetch(0);
   for (int kb = 0; kb < nkeys; kb += PF_KT) {
-    // stage K [key][dim] and V^T [dim][key], then fetch the next tile
+    // stage K [key][dim] and V^T [dim][key] (prefix form: then fetch the next tile)
+    if constexpr (!PREFIX_ONLY) fetch(kb);
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = threadIdx.x + NT * i;
@@ -739,7 +741,8 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       }
     }
     __syncthreads();
-    if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
+    if constexpr (PREFIX_ONLY)
+      if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
     // S^T for key tiles 0 (keys kb..kb+15) and 1 (kb+16..kb+31)
     f32x4 st[2];
 #pragma unroll
