@@ -35,6 +35,8 @@ CASES = [
     ("bf16", 128, 32, 8, 512, 256, 1, 128),
     ("bf16", 128, 64, 8, 300, 256, 0, 16),
     ("bf16", 128, 16, 8, 129, 40, 300, 320),
+    ("bf16", 128, 8, 8, 130, 70, 33, 40),         # one query head per KV head; prefix not a multiple of 64
+    ("bf16", 128, 32, 8, 160, 600, 10, 16),       # prefix longer than the stage ring
     ("bf16", 128, 64, 8, 12, 100, 90, 96),
     ("bf16", 128, 32, 8, 17, 0, 77, 80),
     ("bf16", 128, 32, 8, 5, 256, 0, 16),
