@@ -399,11 +399,16 @@ static int decode_kps(int rows, int hkv, int keys) {
   return (keys + splits - 1) / splits;
 }
 
-// Keys per split for the MFMA streaming kernel: about two work-groups per
-// CU, at least 64 keys per split.
+// Keys per split for the MFMA streaming kernel: as many splits as keep the
+// grid within one round of resident work-groups (two per CU), at least 64
+// keys per split (a partly filled second round measured slower).
 static int tail_mfma_kps(int rows, int hkv, int keys) {
+  static const int target = [] {
+    const char* e = getenv("SPECREJ_TAIL_WG_TARGET");
+    return e ? atoi(e) : 512;
+  }();
   const int64_t groups = (int64_t)rows * hkv;
-  int splits = (int)std::max<int64_t>(1, (512 + groups - 1) / groups);
+  int splits = (int)std::max<int64_t>(1, target / groups);
   splits = std::max(1, std::min(splits, keys / 64));
   return (keys + splits - 1) / splits;
 }
