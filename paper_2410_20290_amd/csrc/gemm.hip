@@ -78,6 +78,133 @@ static inline dim3 tile_grid(int nm, int nn, int splits) {
   return dim3(8 * ((total + 7) / 8));
 }
 
+// ------------------------------------------------------------ tile epilogue
+// The 32x32x16 kernels below multiply with the weight fragment as the first
+// MFMA operand, so each wave accumulates the transpose of its output tile:
+// element e of lane l of acc[i][j] is tile row 32 i + l % 32, tile column
+// 32 j + 8 (e / 4) + 4 (l / 32) + e % 4, i.e. runs of four consecutive
+// columns.  A wave writes its tile as 16-byte chunks (four floats) into its
+// own 32 KB of the then idle LDS, 8192 / CL rows per pass (CL floats per
+// row, chunk c of row r in slot c ^ key(r)), and reads it back along rows,
+// so that global stores (and residual reads) are contiguous row runs of 16
+// (fp32) or 8 (bf16) bytes per lane rather than scattered single elements.
+//
+// Paired tiles: acc[i][2 jj] holds the gate and acc[i][2 jj + 1] the up
+// projection of output columns 32 jj + ...; without partials the SwiGLU
+// product is staged (MERGE, CL = 16 TJ); with partials gate and up are
+// staged side by side (CL = 32 TJ) and go to columns n and N + n of the
+// [split][M][2N] partial rows.
+template <int CL>
+__device__ __forceinline__ int stage_slot(int r, int c) {
+  constexpr int CPR = CL / 4, RB = CL * 4;  // chunks and bytes per row
+  const int key = RB >= 256 ? r % CPR : (r / (256 / RB)) % CPR;
+  return r * CL + 4 * (c ^ key);
+}
+
+__device__ __forceinline__ void store4(float* dst, f32x4 v) { *reinterpret_cast<f32x4*>(dst) = v; }
+
+__device__ __forceinline__ void store4(bf16_t* dst, f32x4 v) {
+  const uint32_t lo = f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+  const uint32_t hi = f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+  *reinterpret_cast<uint2*>(dst) = uint2{lo, hi};
+}
+
+// row0, col0: output row and output column of the wave tile's first row and
+// column (for paired tiles the SwiGLU / partial column, not the weight row).
+// Wave tiles wholly inside the output with 16-byte aligned rows take the
+// unrolled path (residual rows of a pass loaded before its staging); edge
+// tiles store element by element.
+template <int TI, int TJ, bool PAIRED, bool MERGE>
+__device__ __forceinline__ void tile_epilogue_32(const f32x16 (&acc)[TI][TJ], float* st, int lane, int row0,
+                                                 int col0, int M, int N, int split, const EpiArgs& epi,
+                                                 float* __restrict__ partial) {
+  static_assert(!MERGE || PAIRED, "only paired tiles merge gate and up");
+  constexpr int CL = MERGE ? 16 * TJ : 32 * TJ;                 // staged floats per row
+  constexpr int LPR = CL / 4;                                   // lanes per row on read-back
+  constexpr int RPI = 64 / LPR;                                 // rows per read-back instruction
+  constexpr int RP = 8192 / CL < 32 * TI ? 8192 / CL : 32 * TI;  // rows per pass
+  constexpr int NP = 32 * TI / RP, NQ = RP / RPI;
+  constexpr int WCOLS = PAIRED ? 16 * TJ : 32 * TJ;             // output columns of the wave tile
+  static_assert(LPR <= 64 && RP % 32 == 0 && RP % RPI == 0, "epilogue shape");
+  const int lr = lane & 31, lh = lane >> 5;
+  const int rr = lane / LPR, cc = 4 * (lane % LPR);  // read-back row within a group, staged column
+
+  // staged column cc -> output column n (and the gate or up half of a
+  // paired partial row)
+  int n = col0 + cc;
+  bool up = false;
+  if (PAIRED && !MERGE) {
+    const int j = cc / 32;
+    n = col0 + 32 * (j / 2) + cc % 32;
+    up = j & 1;
+  }
+  const bool to_part = partial != nullptr;
+  const bool resid = !PAIRED && !to_part && epi.mode == EPI_RESID;
+  const bool bf = !to_part && !resid && epi.out_bf16;
+  const int64_t ld = to_part ? (PAIRED ? 2 * (int64_t)N : (int64_t)N) : (int64_t)epi.ldo;
+  const bool aligned = to_part ? (N % 4 == 0 && (reinterpret_cast<uintptr_t>(partial) & 15) == 0)
+                               : (epi.ldo % 4 == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0);
+  const bool interior = aligned && row0 + 32 * TI <= M && col0 + WCOLS <= N;
+  const int64_t col = n + (up ? N : 0);
+  float* const fbase = to_part ? partial + (int64_t)split * M * ld : reinterpret_cast<float*>(epi.out);
+  bf16_t* const bbase = reinterpret_cast<bf16_t*>(epi.out);
+
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int prow = row0 + p * RP;
+    f32x4 old[NQ];
+    if (interior && resid) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        old[q] = *reinterpret_cast<const f32x4*>(fbase + (int64_t)(prow + q * RPI + rr) * ld + col);
+    }
+#pragma unroll
+    for (int ii = 0; ii < RP / 32; ++ii) {
+      const int i = p * (RP / 32) + ii;
+      const int r = ii * 32 + lr;
+#pragma unroll
+      for (int j = 0; j < (MERGE ? TJ / 2 : TJ); ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          f32x4 v;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            if constexpr (MERGE) v[k] = silu(acc[i][2 * j][4 * g + k]) * acc[i][2 * j + 1][4 * g + k];
+            else v[k] = acc[i][j][4 * g + k];
+          }
+          *reinterpret_cast<f32x4*>(st + stage_slot<CL>(r, 8 * j + 2 * g + lh)) = v;
+        }
+    }
+    if (interior) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int r = q * RPI + rr;
+        f32x4 v = *reinterpret_cast<const f32x4*>(st + stage_slot<CL>(r, cc / 4));
+        const int64_t off = (int64_t)(prow + r) * ld + col;
+        if (resid) v += old[q];
+        if (bf) store4(bbase + off, v);
+        else store4(fbase + off, v);
+      }
+    } else {
+#pragma unroll 1
+      for (int q = 0; q < NQ; ++q) {
+        const int r = q * RPI + rr;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(st + stage_slot<CL>(r, cc / 4));
+        const int m = prow + r;
+        if (m >= M) continue;
+        const int64_t off = (int64_t)m * ld + col;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (n + k >= N) break;
+          if (resid) fbase[off + k] += v[k];
+          else if (bf) bbase[off + k] = f32_to_bf16(v[k]);
+          else fbase[off + k] = v[k];
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ bf16 MFMA GEMM
 // Block tile BM x BN (x2 when PAIRED: gate rows n and up rows pair_off + n),
 // K step BK, wave tile WM x WN.  PAIRED epilogue: silu(gate) * up.
@@ -449,7 +576,7 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
   };
   // instruction interleavings: (MFMA, fragment read) x 16; (MFMA, read) x 8
   // then 8 MFMAs; (2 MFMAs, DMA) x 8; (MFMA, read, MFMA, DMA) x 8
@@ -533,68 +660,14 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     if (t + 1 < nk) step(t + 1, a1, b1, a2, b2, a0, b0);
     if (t + 2 < nk) step(t + 2, a2, b2, a0, b0, a1, b1);
   }
-  // no DMA may still be writing LDS when the work-group ends
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
-  if (!PAIRED && !partial && epi.mode == EPI_RESID) {
-    // residual add: all 64 old values of a row block are loaded before any
-    // store, so their latencies overlap
-    float* h = reinterpret_cast<float*>(epi.out);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float old[4][16];
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
-          const int n = n0 + wn0 + j * 32 + fr;
-          old[j][e] = (m < M && n < N) ? h[(int64_t)m * epi.ldo + n] : 0.f;
-        }
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
-          const int n = n0 + wn0 + j * 32 + fr;
-          if (m < M && n < N) h[(int64_t)m * epi.ldo + n] = old[j][e] + acc[i][j][e];
-        }
-    }
-    return;
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
-      if (m >= M) continue;
-      if (PAIRED) {
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int n = n0 + (wn0 >> 1) + jj * 32 + fr;
-          if (n >= N) continue;
-          const float g = acc[i][2 * jj][e], u = acc[i][2 * jj + 1][e];
-          if (partial) {
-            float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
-            p[n] = g;
-            p[N + n] = u;
-          } else {
-            store_out(epi, m, n, silu(g) * u);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int n = n0 + wn0 + j * 32 + fr;
-          if (n >= N) continue;
-          if (partial)
-            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
-          else
-            epi_one(epi, m, n, acc[i][j][e]);
-        }
-      }
-    }
+  // no DMA may still be writing LDS and no wave still reading it
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  float* st = reinterpret_cast<float*>(lds) + wave * 8192;
+  if (PAIRED && !partial)
+    tile_epilogue_32<4, 4, PAIRED, PAIRED>(acc, st, lane, m0 + wm0, n0 + wn0 / 2, M, N, tile.split, epi, partial);
+  else
+    tile_epilogue_32<4, 4, PAIRED, false>(acc, st, lane, m0 + wm0, n0 + (PAIRED ? wn0 / 2 : wn0), M, N, tile.split,
+                                          epi, partial);
 }
 #undef SR_VM_BARRIER
 
@@ -688,7 +761,7 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
   };
   // quarters 0-2: (MFMA, read, MFMA, DMA) x 4, then the last two reads
   auto reads_dmas = [] {
@@ -750,39 +823,14 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
     mfma(a1, b1);
     reads();
   }
-  // no DMA may still be writing LDS when the work-group ends
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-  // 32x32 accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + wm0 + i * 32 + 8 * (e >> 2) + 4 * fg + (e & 3);
-      if (m >= M) continue;
-      if (PAIRED) {
-        const int n = n0 + (wn0 >> 1) + fr;
-        if (n >= N) continue;
-        const float g = acc[i][0][e], u = acc[i][1][e];
-        if (partial) {
-          float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
-          p[n] = g;
-          p[N + n] = u;
-        } else {
-          store_out(epi, m, n, silu(g) * u);
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int n = n0 + wn0 + j * 32 + fr;
-          if (n >= N) continue;
-          if (partial)
-            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][j][e];
-          else
-            epi_one(epi, m, n, acc[i][j][e]);
-        }
-      }
-    }
+  // no DMA may still be writing LDS and no wave still reading it
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  float* st = reinterpret_cast<float*>(lds) + wave * 8192;
+  if (PAIRED && !partial)
+    tile_epilogue_32<4, 2, PAIRED, PAIRED>(acc, st, lane, m0 + wm0, n0 + wn0 / 2, M, N, tile.split, epi, partial);
+  else
+    tile_epilogue_32<4, 2, PAIRED, false>(acc, st, lane, m0 + wm0, n0 + (PAIRED ? wn0 / 2 : wn0), M, N, tile.split,
+                                          epi, partial);
 }
 #undef SR_VMB3
 
