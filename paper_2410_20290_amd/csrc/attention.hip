@@ -219,8 +219,9 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
 // Decode attention over keys [key0, P + lt) for bf16, head_dim 128, on
 // MFMA.  Work-group = (split, KV head, row), 4 waves; the G query heads of
 // the KV head are the 16 columns of v_mfma_f32_16x16x32_bf16 (columns >= G
-// are zero queries whose results are dropped).  Stage = 64 keys of K and V
-// (32 KB) copied into LDS with global_load_lds_dwordx4, one stage ahead.
+// are zero queries whose results are dropped).  Stage = SK keys of K and V
+// (SK / 2 KB) copied into LDS with global_load_lds_dwordx4, NST - 1 stages
+// ahead.
 // Per 32 keys every wave computes
 //   S^T = K Q^T   (two 16-key tiles): lane l holds keys 4(l/16)+i and
 //                 16+4(l/16)+i of query l%16 (all waves alike),
@@ -232,14 +233,28 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
 // LDS rows of 256 bytes (16 chunks of 8 dims): K chunk c of key k sits in
 // slot c ^ (k & 15), V chunk c in slot c ^ 2 ((k >> 2) & 3), so both read
 // patterns are free of bank conflicts.
-template <int G>
-__global__ void __launch_bounds__(256)
+// Wait until at most N vector-memory operations of this wave are in flight,
+// then meet the other waves.
+template <int N>
+__device__ __forceinline__ void tail_stage_wait() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else static_assert(N < 0, "add this wait count");
+}
+
+template <int G, int SK, int NST>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SK == 32 ? 4 : 1)))
 decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
                         int P, const bf16_t* __restrict__ ktail, const bf16_t* __restrict__ vtail, int cap, int lt,
                         int hq, int hkv, int kps, int splits, float* __restrict__ part, bf16_t* __restrict__ out,
                         float qscale, int key0, int split0) {
-  constexpr int HD = 128, SK = 64, NST = 2;
+  constexpr int HD = 128;
   constexpr int STAGE = 2 * SK * HD;  // bf16 elements: K rows then V rows
+  constexpr int DI = SK / 16;         // DMA instructions per wave per stage, for K and again for V
+  static_assert(SK % 32 == 0 && NST >= 2, "stage shape");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
   const int split = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
   const int lane = threadIdx.x & 63;
@@ -259,7 +274,7 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
   auto issue = [&](int st, int buf) {
     bf16_t* dst = lds + buf * STAGE;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < DI; ++i) {
       const int kr = 4 * (wave + 4 * i) + fg;  // key row in the stage
       const int j = min(k0 + min(st, nst - 1) * SK + kr, k1 - 1);
       const int64_t rowoff = (int64_t)(j < P ? j : j - P) * HD;
@@ -284,14 +299,20 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
   // V^T reads: dimension 32 wave + 16 dt + fr, keys 4 fg + i (+ 16)
   const int vdim0 = 32 * wave + fr;
 
-  issue(0, 0);
-  for (int t = 0; t < nst; ++t) {
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    issue(t + 1, (t + 1) & 1);
-    const bf16_t* ks = lds + (t & 1) * STAGE;
-    const bf16_t* vs = ks + SK * HD;
+  // stages 0 .. NST - 2 ahead; every step then refills the buffer of the
+  // step before (past the last stage the last one is fetched again, unused),
+  // so every wait is the same
 #pragma unroll
-    for (int tp = 0; tp < 2; ++tp) {
+  for (int st = 0; st < NST - 1; ++st) issue(st, st);
+  int cur = 0;  // buffer of step t
+  for (int t = 0; t < nst; ++t) {
+    tail_stage_wait<(NST - 2) * 2 * DI>();
+    issue(t + NST - 1, cur == 0 ? NST - 1 : cur - 1);
+    const bf16_t* ks = lds + cur * STAGE;
+    const bf16_t* vs = ks + SK * HD;
+    cur = cur == NST - 1 ? 0 : cur + 1;
+#pragma unroll
+    for (int tp = 0; tp < SK / 32; ++tp) {
       f32x4 st[2];
 #pragma unroll
       for (int kt2 = 0; kt2 < 2; ++kt2) {
@@ -454,10 +475,19 @@ static bool tail_by_mfma(int dtype, int hd, int g, int rows) {
 template <int G>
 static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsplit, int splits, int split0,
                              float qscale, hipStream_t s) {
-  hipLaunchKernelGGL((decode_tail_mfma_kernel<G>), dim3(nsplit, a.hkv, a.rows), dim3(256), 0, s, a.q,
-                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.ktail,
-                     (const bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out,
-                     qscale, key0, split0);
+#define SR_TAIL(SK, NST)                                                                                        \
+  hipLaunchKernelGGL((decode_tail_mfma_kernel<G, SK, NST>), dim3(nsplit, a.hkv, a.rows), dim3(256), 0, s, a.q, \
+                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.ktail,                  \
+                     (const bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out,      \
+                     qscale, key0, split0)
+  // 64-key stages hold 2 work-groups per CU (registers and LDS), 32-key
+  // stages 4: the latter when one work-group per (row, KV head) alone
+  // exceeds a round of the former (more resident waves to hide the
+  // dependent MFMA / softmax chain); the former, with fewer barriers per
+  // key, otherwise
+  if ((int64_t)a.rows * a.hkv > 2 * 256) SR_TAIL(32, 2);
+  else SR_TAIL(64, 2);
+#undef SR_TAIL
   SR_CHECK_LAUNCH();
 }
 
