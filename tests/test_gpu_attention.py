@@ -33,6 +33,7 @@ CASES = [
     ("bf16", 128, 32, 8, 160, 256, 20, 32),
     ("bf16", 128, 32, 8, 512, 256, 127, 128),     # first round of the 8B schedule
     ("bf16", 128, 32, 8, 512, 256, 1, 128),
+    ("bf16", 128, 32, 8, 1024, 256, 33, 40),      # largest row count of the MFMA streaming form
     ("bf16", 128, 64, 8, 300, 256, 0, 16),
     ("bf16", 128, 16, 8, 129, 40, 300, 320),
     ("bf16", 128, 8, 8, 130, 70, 33, 40),         # one query head per KV head; prefix not a multiple of 64
