@@ -248,9 +248,10 @@ __device__ __forceinline__ void tail_stage_wait() {
 template <int G, int SK, int NST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SK == 32 ? 4 : 1)))
 decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
-                        int P, const bf16_t* __restrict__ ktail, const bf16_t* __restrict__ vtail, int cap, int lt,
+                        int P, bf16_t* ktail, bf16_t* vtail, int cap, int lt,
                         int hq, int hkv, int kps, int splits, float* __restrict__ part, bf16_t* __restrict__ out,
-                        float qscale, int key0, int split0) {
+                        float qscale, int key0, int split0, const float* __restrict__ qpart, int qsplits,
+                        int qkv_dim, const float2* __restrict__ rope, float* __restrict__ qout) {
   constexpr int HD = 128;
   constexpr int STAGE = 2 * SK * HD;  // bf16 elements: K rows then V rows
   constexpr int DI = SK / 16;         // DMA instructions per wave per stage, for K and again for V
@@ -284,15 +285,34 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
     }
   };
 
-  // Q^T fragments (B operand): lane holds Q[query fr][32 s + 8 fg .. + 8], scaled, bf16
-  bf16x8 qf[4];
-  {
-    const bool qvalid = fr < G;
-    const float* qr = q + ((int64_t)row * hq + h * G + (qvalid ? fr : 0)) * HD;
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)(qvalid ? qr[32 * s + 8 * fg + e] * qscale : 0.f);
+  // Fused QKV finalize.  The work-group that holds the newest key (response
+  // index lt - 1) writes its K (rotated) and V row first; vector-memory
+  // operations of a wave complete in issue order, so the wait before any
+  // later DMA of that row (the prologue's below, else a step's wait plus
+  // barrier) also covers these stores.
+  const bool writer = qpart && k1 == total;
+  if (writer && wave == 0) {
+    const int64_t qs = (int64_t)gridDim.z * qkv_dim;
+    const float* pk = qpart + (int64_t)row * qkv_dim + (hq + h) * HD;
+    const float* pv = pk + hkv * HD;
+    float k1v = 0.f, k2v = 0.f, v1 = 0.f, v2 = 0.f;
+    for (int sp = 0; sp < qsplits; ++sp) {
+      k1v += pk[sp * qs + lane];
+      k2v += pk[sp * qs + 64 + lane];
+      v1 += pv[sp * qs + lane];
+      v2 += pv[sp * qs + 64 + lane];
+    }
+    const float2 c = rope[lane];
+    const int64_t at = (((int64_t)row * hkv + h) * cap + lt - 1) * HD;
+    ktail[at + lane] = f32_to_bf16(k1v * c.x - k2v * c.y);
+    ktail[at + 64 + lane] = f32_to_bf16(k2v * c.x + k1v * c.y);
+    vtail[at + lane] = f32_to_bf16(v1);
+    vtail[at + 64 + lane] = f32_to_bf16(v2);
+  }
+  if (writer && nst - 1 <= NST - 2) {
+    // the newest key is in a prologue stage
+    if (wave == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
   }
   f32x4 o[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
   float m = -INFINITY, l = 0.f;
@@ -304,6 +324,65 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
   // so every wait is the same
 #pragma unroll
   for (int st = 0; st < NST - 1; ++st) issue(st, st);
+
+  // Q^T fragments (B operand): lane holds Q[query fr][32 s + 8 fg .. + 8],
+  // scaled, bf16; loaded under the prologue's DMAs.  Fused: the partials of
+  // dimensions d and d + 64 (a rotation pair) are the lane's s and s + 2.
+  bf16x8 qf[4];
+  {
+    const bool qvalid = fr < G;
+    const int qh = h * G + (qvalid ? fr : 0);
+    if (qpart) {
+      const int64_t qs = (int64_t)gridDim.z * qkv_dim;
+      const float* pq = qpart + (int64_t)row * qkv_dim + qh * HD + 8 * fg;
+      f32x4 x[2][2][2];  // [s][half][four of eight]
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+          for (int f = 0; f < 2; ++f) x[s][hf][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (qvalid)
+        for (int sp = 0; sp < qsplits; ++sp) {
+          f32x4 y[2][2][2];
+#pragma unroll
+          for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+              for (int f = 0; f < 2; ++f)
+                y[s][hf][f] = *reinterpret_cast<const f32x4*>(pq + sp * qs + 64 * hf + 32 * s + 4 * f);
+#pragma unroll
+          for (int s = 0; s < 2; ++s)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+              for (int f = 0; f < 2; ++f) x[s][hf][f] += y[s][hf][f];
+        }
+      float* qo = qout && split == 0 && wave == 0 && qvalid ? qout + ((int64_t)row * hq + qh) * HD : nullptr;
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int d = 32 * s + 8 * fg + e;
+          const float x1 = x[s][0][e >> 2][e & 3], x2 = x[s][1][e >> 2][e & 3];
+          const float2 c = rope[d];
+          const float y1 = x1 * c.x - x2 * c.y, y2 = x2 * c.x + x1 * c.y;
+          qf[s][e] = (__bf16)(qvalid ? y1 * qscale : 0.f);
+          qf[s + 2][e] = (__bf16)(qvalid ? y2 * qscale : 0.f);
+          if (qo) {
+            qo[d] = y1;
+            qo[64 + d] = y2;
+          }
+        }
+    } else {
+      const float* qr = q + ((int64_t)row * hq + qh) * HD;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)(qvalid ? qr[32 * s + 8 * fg + e] * qscale : 0.f);
+    }
+  }
   int cur = 0;  // buffer of step t
   for (int t = 0; t < nst; ++t) {
     tail_stage_wait<(NST - 2) * 2 * DI>();
@@ -478,9 +557,9 @@ static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsp
                              float qscale, hipStream_t s) {
 #define SR_TAIL(SK, NST)                                                                                        \
   hipLaunchKernelGGL((decode_tail_mfma_kernel<G, SK, NST>), dim3(nsplit, a.hkv, a.rows), dim3(256), 0, s, a.q, \
-                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.ktail,                  \
-                     (const bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out,      \
-                     qscale, key0, split0)
+                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail,      \
+                     a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out, qscale, key0, split0,        \
+                     a.qpart, a.qsplits, a.qkv_dim, a.rope, a.qout)
   // 64-key stages hold 2 work-groups per CU (registers and LDS), 32-key
   // stages 4: the latter when one work-group per (row, KV head) alone
   // exceeds a round of the former (more resident waves to hide the
@@ -508,6 +587,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     // the streaming kernel over the keys past the prefix pass's, then the
     // prefix pass or (several splits without it) the merge
     const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
+    SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), 3, "fused QKV finalize needs a new key");
     const int key0 = pre ? a.P : 0;
     const int keys = a.P + a.lt - key0;
     const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
@@ -519,6 +599,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     if (tsplits > 0) {
       DecodeAttnArgs b = a;
       if (!direct) b.out = nullptr;
+      if (!pre) b.qout = nullptr;  // only the prefix pass reads q back
       launch_tail_mfma<G>(b, key0, kps, tsplits, tsplits, 0, qscale, s);
     }
     if (pre) {
@@ -530,6 +611,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     }
     return;
   }
+  SR_REQUIRE(!a.qpart, SR_ERR_INTERNAL, "fused QKV finalize without the streaming kernel");
   if (prefix_by_mfma(a.dtype, HD, a.P, a.rows)) {
     // tail partials, then the prefix pass
     const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;
@@ -582,6 +664,14 @@ static void decode_by_hd(const DecodeAttnArgs& a, hipStream_t s) {
     case 128: decode_by_group<T, 128>(a, s); break;
     default: SR_REQUIRE(false, 3, "head_dim must be 32, 64 or 128");
   }
+}
+
+// Whether decode_attn sums the QKV partials itself (the MFMA streaming form:
+// bf16, head_dim 128, 1, 2, 4 or 8 query heads per KV head).
+bool decode_attn_fuses_qkv(const DecodeAttnArgs& a) {
+  if (a.hkv <= 0 || a.hq % a.hkv) return false;
+  const int g = a.hq / a.hkv;
+  return (g == 1 || g == 2 || g == 4 || g == 8) && a.lt >= 1 && tail_by_mfma(a.dtype, a.hd, g, a.rows);
 }
 
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s) {

@@ -499,18 +499,26 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
     char* kpool = (char*)pool + (size_t)(2 * l) * pool_block * m.es;
     char* vpool = (char*)pool + (size_t)(2 * l + 1) * pool_block * m.es;
     int sp = run_gemm(c, true, m.dtype, L.xn, m.d, G.wqkv(l), m.d, rows, m.qkv, m.d, EPI_PARTIAL, nullptr, 0, 0);
-    run_other(c, (double)rows * (m.qkv * 4.0 * sp + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es), [&] {
-      qkv_finalize(m.dtype, L.gpart, sp, rows, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool, vpool,
-                   cap, step - 1, c.s);
-    });
     DecodeAttnArgs a;
     a.dtype = m.dtype; a.hd = m.hd; a.hq = m.hq; a.hkv = m.hkv; a.rows = rows; a.q = L.q;
     a.kpre = (const char*)L.gpre + l * pre_lay;
     a.vpre = (const char*)L.gpre + l * pre_lay + pre_lay / 2;
     a.P = pl.P; a.ktail = kpool; a.vtail = vpool; a.cap = cap; a.lt = step; a.out = L.o;
     a.part = L.apart; a.part_cap = pl.apart;
+    // the QKV partials are summed, rotated and scattered inside the
+    // attention where its streaming form runs, else by their own kernel
+    a.qpart = L.gpart; a.qsplits = sp; a.qkv_dim = m.qkv;
+    a.rope = L.rope_g + (size_t)(pl.P + step - 1) * (m.hd / 2); a.qout = L.q;
+    const double qbytes = (double)rows * (m.qkv * 4.0 * sp + m.hq * m.hd * 4.0 + 2.0 * m.hkv * m.hd * m.es);
+    if (!decode_attn_fuses_qkv(a)) {
+      a.qpart = nullptr;
+      run_other(c, qbytes, [&] {
+        qkv_finalize(m.dtype, L.gpart, sp, rows, m.hq, m.hkv, m.hd, L.rope_g, pl.P + step - 1, L.q, kpool, vpool,
+                     cap, step - 1, c.s);
+      });
+    }
     const double abytes = 2.0 * m.hkv * m.hd * m.es * ((double)pl.P + (double)rows * step) +
-                          (double)rows * m.hq * m.hd * (4 + m.es);
+                          (double)rows * m.hq * m.hd * (4 + m.es) + (a.qpart ? qbytes : 0.0);
     const double aflops = 4.0 * rows * m.hq * m.hd * ((double)pl.P + step);
     timed(c, SR_K_DECODE_ATTN, abytes, aflops, [&] { decode_attn(a, c.s); });
     sp = run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_PARTIAL,

@@ -91,8 +91,19 @@ struct DecodeAttnArgs {
   void* out;
   float* part;       // split partials [rows][hq][splits][hd + 2]
   size_t part_cap;   // floats
+  // Fused QKV finalize (decode_attn_fuses_qkv): instead of q, the QKV
+  // projection's split partials qpart [qsplits][rows][qkv_dim] are summed
+  // here; q and k heads are rotated with rope[hd / 2] (the table row of the
+  // new position); the new K/V row is written to ktail/vtail at index lt - 1
+  // before it is attended, and the rotated fp32 q to qout (for the prefix
+  // pass) when qout is set.
+  const float* qpart = nullptr;
+  int qsplits = 0, qkv_dim = 0;
+  const float2* rope = nullptr;
+  float* qout = nullptr;
 };
 int decode_attn_splits(int rows, int hkv, int keys);
+bool decode_attn_fuses_qkv(const DecodeAttnArgs& a);
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s);
 
 // Prefill: rows of lr new tokens that follow t0 tokens already cached for
