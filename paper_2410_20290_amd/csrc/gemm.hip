@@ -942,7 +942,7 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j)
-          acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[b][j], acc[b][i][j], 0, 0, 0);
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[b][j], af[i], acc[b][i][j], 0, 0, 0);
   };
   // one MFMA, then one fragment read of the next sub-step, alternating;
   // then the remaining MFMAs
@@ -1008,27 +1008,60 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   // no DMA may still be writing LDS when the work-group ends
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-  // Accumulator layout: lane holds rows 4*(lane/16) + e, column lane % 16.
+  // The weight fragment is the first MFMA operand, so the accumulators hold
+  // the transposed tile: lane l has row 16 i + l % 16 and the four
+  // consecutive columns 16 j + 4 (l / 16) .. + 3, stored as one 16-byte
+  // (fp32) or 8-byte (bf16) chunk where the row is aligned and the columns
+  // are inside the output.
+  const int mrow = m0 + wm0 + fr, ncol = n0 + wn0 + 4 * fg;
+  const bool to_part = partial != nullptr;
+  const bool resid = !PAIRED && !to_part && epi.mode == EPI_RESID;
+  const bool bf = !to_part && !resid && epi.out_bf16;
+  const int64_t ld = to_part ? (int64_t)NB * N : (int64_t)epi.ldo;
+  const bool aligned = to_part ? (N % 4 == 0 && (reinterpret_cast<uintptr_t>(partial) & 15) == 0)
+                               : (epi.ldo % 4 == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0);
+  float* const fbase = to_part ? partial + (int64_t)tile.split * M * ld : reinterpret_cast<float*>(epi.out);
+  bf16_t* const bbase = reinterpret_cast<bf16_t*>(epi.out);
 #pragma unroll
-  for (int i = 0; i < TI; ++i)
+  for (int i = 0; i < TI; ++i) {
+    const int m = mrow + 16 * i;
+    if (m >= M) continue;
 #pragma unroll
-    for (int j = 0; j < TJ; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = m0 + wm0 + i * 16 + fg * 4 + e;
-        const int n = n0 + wn0 + j * 16 + fr;
-        if (m >= M || n >= N) continue;
-        if (partial) {
-          const int nout = NB * N;
-          float* p = partial + ((int64_t)tile.split * M + m) * nout;
-          p[n] = acc[0][i][j][e];
-          if (PAIRED) p[N + n] = acc[NB - 1][i][j][e];
-        } else if (PAIRED) {
-          store_out(epi, m, n, silu(acc[0][i][j][e]) * acc[NB - 1][i][j][e]);
+    for (int j = 0; j < TJ; ++j) {
+      const int n = ncol + 16 * j;
+      if (n >= N) continue;
+      const bool full = aligned && n + 3 < N;
+      const int64_t off = (int64_t)m * ld + n;
+      f32x4 v = acc[0][i][j];
+      if (to_part) {
+        if (full) {
+          store4(fbase + off, v);
+          if (PAIRED) store4(fbase + off + N, acc[NB - 1][i][j]);
         } else {
-          epi_one(epi, m, n, acc[0][i][j][e]);
+          for (int k = 0; k < 4 && n + k < N; ++k) {
+            fbase[off + k] = v[k];
+            if (PAIRED) fbase[off + N + k] = acc[NB - 1][i][j][k];
+          }
+        }
+        continue;
+      }
+      if (PAIRED) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = silu(v[k]) * acc[NB - 1][i][j][k];
+      }
+      if (full) {
+        if (resid) v += *reinterpret_cast<const f32x4*>(fbase + off);
+        if (bf) store4(bbase + off, v);
+        else store4(fbase + off, v);
+      } else {
+        for (int k = 0; k < 4 && n + k < N; ++k) {
+          if (resid) fbase[off + k] += v[k];
+          else if (bf) bbase[off + k] = f32_to_bf16(v[k]);
+          else fbase[off + k] = v[k];
         }
       }
+    }
+  }
 }
 #undef SR_VMB
 
