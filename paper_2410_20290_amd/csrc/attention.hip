@@ -781,10 +781,28 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 //   O^T += V^T P^T (dims x queries): the key order of this contraction is
 //                 permuted so that the B operand is exactly the lane's own
 //                 S^T values (keys 4g..4g+3 of tile 0, then of tile 1); the A
-//                 operand reads V^T, staged transposed in LDS, at those keys.
+//                 operand comes from the V tile, staged row by row like K, by
+//                 two LDS transpose reads.
 constexpr int PF_KT = 32;            // keys per tile
 constexpr int PF_KROW = 128 + 8;     // K tile row (bf16), padded
-constexpr int PF_VROW = 32 + 4;      // V^T tile row (bf16), padded
+constexpr int PF_VROW = 128 + 16;    // V tile row (bf16), padded: the 8-byte transpose reads of a
+                                     // half wave (eight rows) fall on distinct banks
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Every lane names 8 bytes
+// (four bf16); within each group of 16 lanes, element e of lane i's result
+// is element (i & 3) of the four named by lane 4 e + (i >> 2).
+__device__ __forceinline__ i16x4 lds_read_tr16(const bf16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+// two transpose reads as one MFMA operand (the 16-bit words reinterpreted
+// as a whole vector)
+__device__ __forceinline__ bf16x8 tr16_pair(i16x4 lo, i16x4 hi) {
+  const i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, w);
+}
 
 // PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
 // The 16 "queries" of a work-group are 16 decode rows (lr = rows, one
@@ -803,7 +821,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
                          bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
   constexpr int HD = 128, NT = 64 * G;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[HD * PF_VROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[PF_KT * PF_VROW];
   const int qb = blockIdx.x, h = blockIdx.y, row = PREFIX_ONLY ? 0 : blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fg = lane >> 4;
@@ -859,12 +877,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       if (c >= PF_KT * 16) break;
       const int j = c >> 4, cc = c & 15;
       *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
-      const uint32_t w4[4] = {vreg[i].x, vreg[i].y, vreg[i].z, vreg[i].w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(cc * 8 + 2 * e) * PF_VROW + j] = (bf16_t)(w4[e] & 0xFFFFu);
-        Vt[(cc * 8 + 2 * e + 1) * PF_VROW + j] = (bf16_t)(w4[e] >> 16);
-      }
+      *reinterpret_cast<uint4*>(&Vs[j * PF_VROW + cc * 8]) = vreg[i];
     }
     __syncthreads();
     if constexpr (PREFIX_ONLY)
@@ -909,16 +922,17 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     ls += __shfl_xor(ls, 32, 64);
     l = l * corr + ls;
     m = mn;
-    // O^T += V^T P^T over the 32 keys in the permuted order
+    // O^T += V^T P^T over the 32 keys in the permuted order.  Lane i of a
+    // group names dims dt 16 + 4 (i & 3) .. + 3 of key 4 fg + (i >> 2) (and
+    // 16 keys on), so it receives dim dt 16 + i of keys 4 fg .. + 3 (and
+    // 16 + 4 fg .. + 3): the A operand rows
+    const bf16_t* vb = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
       o[dt] *= corr;
-      const bf16_t* vr = &Vt[(dt * 16 + fr) * PF_VROW];
-      const uint2 a0 = *reinterpret_cast<const uint2*>(vr + 4 * fg);
-      const uint2 a1 = *reinterpret_cast<const uint2*>(vr + 16 + 4 * fg);
-      const uint4 a = make_uint4(a0.x, a0.y, a1.x, a1.y);
-      const bf16x8 vf = *reinterpret_cast<const bf16x8*>(&a);
-      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[dt], 0, 0, 0);
+      const i16x4 lo = lds_read_tr16(vb + dt * 16);
+      const i16x4 hi = lds_read_tr16(vb + 16 * PF_VROW + dt * 16);
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tr16_pair(lo, hi), pf, o[dt], 0, 0, 0);
     }
     __syncthreads();
   }
