@@ -497,7 +497,12 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // banks.
 #define SR_VM_BARRIER(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
-template <bool PAIRED>
+//
+// BRING = 3 (a few hundred rows, where every weight tile comes from HBM and
+// is shared by few row tiles): the weight rows get a ring of three buffers
+// of their own, filled three steps ahead, while the activation rows (in L2)
+// keep two; 160 KB of LDS.
+template <bool PAIRED, int BRING>
 __global__ void __launch_bounds__(256)
 gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
                 int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
@@ -505,7 +510,12 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   constexpr int BM = 256, BNL = 256, BK = 64;
   constexpr int BN_OUT = PAIRED ? 128 : 256;
   constexpr int STAGE = (BM + BNL) * BK;  // bf16 elements per stage
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE];
+  constexpr int HALF = BM * BK;           // bf16 elements of the A (or B) rows of a stage
+  static_assert(BRING == 2 || BRING == 3, "weight ring depth");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[BRING == 2 ? 2 * STAGE : 2 * HALF + 3 * HALF];
+  // A rows of ring slot `a`, B rows of ring slot `b`
+  auto a_base = [&](int a) { return lds + (BRING == 2 ? a * STAGE : a * HALF); };
+  auto b_base = [&](int b) { return lds + (BRING == 2 ? b * STAGE + HALF : 2 * HALF + b * HALF); };
 
   const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN_OUT - 1) / BN_OUT, K / k_per_split);
   if (!tile.valid) return;
@@ -539,10 +549,10 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   }
   const char* Ab = reinterpret_cast<const char*>(A + k_begin);
   const char* Bb = reinterpret_cast<const char*>(B + k_begin);
-  // half h of stage `st` into buffer `buf`: the A rows (h = 0) or the B rows
-  // (h = 1), 8 instructions per wave
+  // half h of stage `st` into ring slot `buf`: the A rows (h = 0) or the B
+  // rows (h = 1), 8 instructions per wave
   auto issue_half = [&](int st, int buf, int h) {
-    bf16_t* dst = lds + buf * STAGE + h * BM * BK;
+    bf16_t* dst = h ? b_base(buf) : a_base(buf);
     const char* src = (h ? Bb : Ab) + st * BK * 2;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
@@ -556,12 +566,13 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   int foff[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) foff[q] = fr * BK + 8 * ((2 * q + fg) ^ sw);
-  auto read_frags = [&](int buf, int q, bf16x8(&af)[4], bf16x8(&bfr)[4]) {
-    const bf16_t* sa = lds + buf * STAGE + foff[q];
+  auto read_frags = [&](int abuf, int bbuf, int q, bf16x8(&af)[4], bf16x8(&bfr)[4]) {
+    const bf16_t* sa = a_base(abuf) + foff[q];
+    const bf16_t* sb = b_base(bbuf) + foff[q];
 #pragma unroll
     for (int i = 0; i < 4; ++i) af[i] = *reinterpret_cast<const bf16x8*>(sa + (wm0 + 32 * i) * BK);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(sa + (BM + wn0 + 32 * j) * BK);
+    for (int j = 0; j < 4; ++j) bfr[j] = *reinterpret_cast<const bf16x8*>(sb + (wn0 + 32 * j) * BK);
   };
 
   f32x16 acc[4][4];
@@ -623,21 +634,27 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   issue_half(0, 0, 1);
   issue_half(min(1, nk - 1), 1, 0);
   issue_half(min(1, nk - 1), 1, 1);
-  SR_VM_BARRIER(16);
+  if constexpr (BRING == 3) {
+    issue_half(min(2, nk - 1), 2, 1);
+    SR_VM_BARRIER(24);
+  } else {
+    SR_VM_BARRIER(16);
+  }
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
   bf16x8 a0[4], b0[4], a1[4], b1[4], a2[4], b2[4];
-  read_frags(0, 0, a0, b0);
+  read_frags(0, 0, 0, a0, b0);
   // One K step with its quarter 0 in (xa, xb); quarter 3 reuses those
-  // registers and the next step's quarter 0 goes to (ya, yb).
-  auto step = [&](int t, bf16x8(&xa)[4], bf16x8(&xb)[4], bf16x8(&ya)[4], bf16x8(&yb)[4], bf16x8(&za)[4],
-                  bf16x8(&zb)[4]) {
+  // registers and the next step's quarter 0 goes to (ya, yb).  bb, bbn: B
+  // ring slots of steps t and t + 1.
+  auto step = [&](int t, int bb, int bbn, bf16x8(&xa)[4], bf16x8(&xb)[4], bf16x8(&ya)[4], bf16x8(&yb)[4],
+                  bf16x8(&za)[4], bf16x8(&zb)[4]) {
     const int buf = t & 1;
-    const int nx = min(t + 2, nk - 1);
-    read_frags(buf, 1, ya, yb);
-    read_frags(buf, 2, za, zb);
+    const int nx = min(t + 2, nk - 1), nxb = min(t + BRING, nk - 1);
+    read_frags(buf, bb, 1, ya, yb);
+    read_frags(buf, bb, 2, za, zb);
     mfma(xa, xb);
     reads16();
-    read_frags(buf, 3, xa, xb);
+    read_frags(buf, bb, 3, xa, xb);
     mfma(ya, yb);
     reads8();
     // every wave has read all of buffer `buf`
@@ -646,19 +663,23 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     issue_half(nx, buf, 0);
     mfma(za, zb);
     dma8();
-    // step t + 1 landed: all but this wave's 8 newest DMAs, in every wave
-    SR_VM_BARRIER(8);
+    // step t + 1 landed: all but this wave's newest DMAs (the A rows just
+    // issued; with BRING = 3 also the B rows of step t + 2), in every wave
+    if constexpr (BRING == 3) SR_VM_BARRIER(16);
+    else SR_VM_BARRIER(8);
     __builtin_amdgcn_sched_barrier(0);
     // (after the last step this reads a stale buffer that is never used)
-    read_frags(buf ^ 1, 0, ya, yb);
-    issue_half(nx, buf, 1);
+    read_frags(buf ^ 1, bbn, 0, ya, yb);
+    issue_half(nxb, bb, 1);
     mfma(xa, xb);
     reads8_dma8();
   };
   for (int t = 0; t < nk; t += 3) {
-    step(t, a0, b0, a1, b1, a2, b2);
-    if (t + 1 < nk) step(t + 1, a1, b1, a2, b2, a0, b0);
-    if (t + 2 < nk) step(t + 2, a2, b2, a0, b0, a1, b1);
+    // B ring slots: t % 3 with three (t is a multiple of 3 here), t % 2 with two
+    const int s0 = BRING == 3 ? 0 : (t & 1), s1 = BRING == 3 ? 1 : s0 ^ 1, s2 = BRING == 3 ? 2 : s0;
+    step(t, s0, s1, a0, b0, a1, b1, a2, b2);
+    if (t + 1 < nk) step(t + 1, s1, s2, a1, b1, a2, b2, a0, b0);
+    if (t + 2 < nk) step(t + 2, s2, BRING == 3 ? 0 : s1, a2, b2, a0, b0, a1, b1);
   }
   // no DMA may still be writing LDS and no wave still reading it
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -1338,6 +1359,16 @@ static int stream_max_rows() {
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
 
+// Tiles of 256 x 256 from which a few hundred rows take that tile with the
+// three-deep weight ring instead of the 256 x 128 tile (0: never).
+static int dma_wide_min_tiles() {
+  static int v = [] {
+    const char* e = getenv("SPECREJ_DMA_WIDE_MIN_TILES");
+    return e ? atoi(e) : 192;
+  }();
+  return v;
+}
+
 // Rows up to which the three-stage 256 x 128 tile is used (above the
 // streaming kernel's rows).
 static int dma3_max_rows() {
@@ -1366,6 +1397,7 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.skinny = false;
   p.dma = false;
   p.dma3 = false;
+  p.dma_bring = 2;
   p.stream = 0;
   p.stream_bn = 0;
   p.stream_bk = 128;
@@ -1380,6 +1412,16 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     while (tiles * splits * 2 <= 256 && K % (splits * 2 * 128) == 0) splits *= 2;
     p.splits = splits;
     return p;
+  }
+  if (M > stream_max_rows() && M <= dma3_max_rows() && K % 64 == 0 && dma_wide_min_tiles() > 0) {
+    // A few hundred rows, a grid of 256 x 256 tiles that alone fills most of
+    // the CUs: that tile with the three-deep weight ring, unsplit.
+    const int64_t wide = (int64_t)((M + 255) / 256) * ((N + (paired ? 127 : 255)) / (paired ? 128 : 256));
+    if (wide >= dma_wide_min_tiles()) {
+      p.dma = true;
+      p.dma_bring = 3;
+      return p;
+    }
   }
   if (M > stream_max_rows() && M <= dma3_max_rows() && K % 64 == 0) {
     // A few hundred rows (the first decode round): 256 x 128 tiles with
@@ -1563,12 +1605,17 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   } else if (plan.dma && dma_offsets_fit(g)) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
-    if (g.paired)
-      hipLaunchKernelGGL(gemm_dma_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
-                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
-    else
-      hipLaunchKernelGGL(gemm_dma_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
-                         (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
+#define SR_DMA(P, R)                                                                                   \
+  hipLaunchKernelGGL((gemm_dma_kernel<P, R>), grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,        \
+                     (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part)
+    if (plan.dma_bring == 3) {
+      if (g.paired) SR_DMA(true, 3);
+      else SR_DMA(false, 3);
+    } else {
+      if (g.paired) SR_DMA(true, 2);
+      else SR_DMA(false, 2);
+    }
+#undef SR_DMA
     SR_CHECK_LAUNCH();
   } else if (plan.big || plan.dma) {
     const int bn_out = g.paired ? 128 : 256;
