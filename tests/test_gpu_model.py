@@ -83,3 +83,27 @@ def test_reward_and_logits_head_dim_128(g):
     for r in range(3):
         refl = og.logits(list(prompt) + list(toks[r, :20]))[len(prompt) - 1: len(prompt) - 1 + 20]
         assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max()
+
+
+def test_teacher_forced_many_rows_head_dim_128():
+    """Decode with enough rows for the 32-key streaming attention, the
+    batched prefix pass and the QKV finalize fused into the attention (head
+    dim 128, 4 query heads per KV head), checked on a few rows against the
+    oracle."""
+    import synth
+    from oracle.transformer import Transformer
+    torch, sr = need_gpu()
+    shape = _hd128_shape(4)
+    say(f"hd128 many rows shape={shape}")
+    gw, rw = synth.model_weights(shape, 2, False), synth.model_weights(shape, 3, True)
+    gen, rm = sr.DeviceModel.upload(shape, gw, False), sr.DeviceModel.upload(shape, rw, True)
+    prompt = synth.tokens(37, shape.vocab, 6)
+    rows, length = 260, 12
+    toks = np.random.default_rng(7).integers(0, shape.vocab, size=(rows, length)).astype(np.int32)
+    p = sr.make_params(rows, 0.5, length, length)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    lg = sr.logits_teacher_forced(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), ws).cpu().numpy()
+    og = Transformer(shape, gw, False)
+    for r in (0, 131, rows - 1):
+        refl = og.logits(list(prompt) + list(toks[r]))[len(prompt) - 1: len(prompt) - 1 + length]
+        assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max(), r
