@@ -19,7 +19,9 @@ SHAPES = [(1, 64, 64), (17, 100, 128), (33, 1000, 512), (100, 384, 4096), (129, 
           (512, 512, 14336), (1000, 96, 192), (1100, 300, 256), (2048, 520, 1024), (4000, 129, 64),
           (128, 200, 1024), (64, 64, 14336), (21, 4100, 1792), (112, 130, 384),
           # a few hundred rows with enough 256 x 256 tiles for the three-deep weight ring
-          (300, 49152, 256), (257, 24576, 128)]
+          (300, 49152, 256), (257, 24576, 128),
+          # the 103-row QKV projection of the 8B shape (48-column streaming tiles)
+          (103, 6144, 4096)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
