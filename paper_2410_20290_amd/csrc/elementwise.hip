@@ -52,15 +52,75 @@ __global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ 
   for (int i = threadIdx.x; i < d; i += 256) o[i] = from_f32<T>(xr[i] * inv * to_f32<T>(g[i]));
 }
 
+// Four consecutive elements of T.
+__device__ __forceinline__ float4 load4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ float4 load4(const bf16_t* p) {
+  const uint2 u = *reinterpret_cast<const uint2*>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xFFFF0000u));
+}
+__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4(bf16_t* p, float4 v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16),
+                                            f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16));
+}
+
+// Rows whose width is a multiple of 4 and at most 256 KV float4s: the row
+// is loaded once as float4s (all loads in flight together), kept in
+// registers for the scaling pass, and written four elements per store.
+template <typename T, int KV>
+__global__ void __launch_bounds__(256) rmsnorm_vec_kernel(const float* __restrict__ x, int ldx,
+                                                          const T* __restrict__ g, int d, float eps,
+                                                          T* __restrict__ out, int ldo) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, d4 = d / 4;
+  const float* xr = x + (int64_t)r * ldx;
+  float4 v[KV];
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < KV; ++k) {
+    const int j = threadIdx.x + 256 * k;
+    v[k] = j < d4 ? load4(xr + 4 * j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
+  }
+  ss = block_sum256(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  T* o = out + (int64_t)r * ldo;
+#pragma unroll
+  for (int k = 0; k < KV; ++k) {
+    const int j = threadIdx.x + 256 * k;
+    if (j >= d4) continue;
+    const float4 w = load4(g + 4 * j);
+    store4(o + 4 * j, make_float4(v[k].x * inv * w.x, v[k].y * inv * w.y, v[k].z * inv * w.z, v[k].w * inv * w.w));
+  }
+}
+
 void rmsnorm(int dtype, const float* x, int ldx, const void* g, int d, float eps, int rows, void* out,
              int ldo, hipStream_t s) {
   if (rows <= 0) return;
-  if (dtype == SR_BF16)
+  const bool vec = d % 4 == 0 && ldx % 4 == 0 && ldo % 4 == 0 && d <= 4 * 256 * 4 &&
+                   (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(out) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(g) & 15) == 0;
+  const int kv = (d / 4 + 255) / 256;
+#define SR_NORM(T, KV)                                                                                     \
+  hipLaunchKernelGGL((rmsnorm_vec_kernel<T, KV>), dim3(rows), dim3(256), 0, s, x, ldx, (const T*)g, d, eps, \
+                     (T*)out, ldo)
+  if (vec && dtype == SR_BF16) {
+    if (kv <= 1) SR_NORM(bf16_t, 1);
+    else if (kv <= 2) SR_NORM(bf16_t, 2);
+    else SR_NORM(bf16_t, 4);
+  } else if (vec) {
+    if (kv <= 1) SR_NORM(float, 1);
+    else if (kv <= 2) SR_NORM(float, 2);
+    else SR_NORM(float, 4);
+  } else if (dtype == SR_BF16) {
     hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, ldx, (const bf16_t*)g, d,
                        eps, (bf16_t*)out, ldo);
-  else
+  } else {
     hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, x, ldx, (const float*)g, d,
                        eps, (float*)out, ldo);
+  }
+#undef SR_NORM
   SR_CHECK_LAUNCH();
 }
 
