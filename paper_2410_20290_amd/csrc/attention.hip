@@ -216,6 +216,18 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
   }
 }
 
+// Wait until at most N vector-memory operations of this wave are in flight,
+// then meet the other waves.
+template <int N>
+__device__ __forceinline__ void tail_stage_wait() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  else static_assert(N < 0, "add this wait count");
+}
+
 // Decode attention over keys [key0, P + lt) for bf16, head_dim 128, on
 // MFMA.  Work-group = (split, KV head, row), 4 waves; the G query heads of
 // the KV head are the 16 columns of v_mfma_f32_16x16x32_bf16 (columns >= G
@@ -233,18 +245,6 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
 // LDS rows of 256 bytes (16 chunks of 8 dims): K chunk c of key k sits in
 // slot c ^ (k & 15), V chunk c in slot c ^ 2 ((k >> 2) & 3), so both read
 // patterns are free of bank conflicts.
-// Wait until at most N vector-memory operations of this wave are in flight,
-// then meet the other waves.
-template <int N>
-__device__ __forceinline__ void tail_stage_wait() {
-  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else static_assert(N < 0, "add this wait count");
-}
-
 template <int G, int SK, int NST>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SK == 32 ? 4 : 1)))
 decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
@@ -587,7 +587,8 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     // the streaming kernel over the keys past the prefix pass's, then the
     // prefix pass or (several splits without it) the merge
     const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
-    SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), 3, "fused QKV finalize needs a new key");
+    SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), SR_ERR_INTERNAL,
+               "fused QKV finalize needs a new key");
     const int key0 = pre ? a.P : 0;
     const int keys = a.P + a.lt - key0;
     const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;

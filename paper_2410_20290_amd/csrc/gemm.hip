@@ -2,9 +2,11 @@
 // C[m][n] = sum_k A[m][k] * B[n][k], A = activations [M][lda], B = weights
 // [N][ldb] (both K-contiguous), fp32 accumulation, fused epilogues.
 //
-// bf16: MFMA v_mfma_f32_16x16x32_bf16 tiles staged through LDS with double
-// buffering.  fp32: a plain LDS-tiled FMA kernel (used by the fp32 model).
-// Split-K writes fp32 partials [split][M][Nout] that a second kernel sums in
+// bf16: MFMA tiles staged through LDS (by LDS DMA for the main kernels):
+// 256 x 256 and 256 x 128 tiles of v_mfma_f32_32x32x16_bf16 for hundreds of
+// rows and more, streaming tiles of v_mfma_f32_16x16x32_bf16 for up to 128
+// rows.  fp32: a plain LDS-tiled FMA kernel (used by the fp32 model).
+// Split-K writes fp32 partials [split][M][Nout] that a consumer sums in
 // split order, so results do not depend on scheduling.
 #include <cstdlib>
 
