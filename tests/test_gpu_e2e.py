@@ -16,6 +16,17 @@ from oracle import specrej
 
 pytestmark = pytest.mark.gpu
 
+# A head-dim-128 pair small enough for the oracle: its first round (300 rows)
+# runs the 32-key streaming decode attention with the batched prefix pass
+# and the QKV finalize fused into it, the later rounds the 64-key form; two
+# cuts compact the generator's and the reward model's caches.
+import synth  # noqa: E402
+
+synth.CONFIGS.setdefault(
+    "hd128_bf16",
+    synth.RunConfig("hd128_bf16", synth.ModelShape(2, 1024, 8, 2, 128, 512, 1000, "bf16", 500000.0),
+                    40, 300, 16, 0.8, 128))
+
 
 def gpu_run(name, reward_kind=0, reward_recompute=0, **over):
     torch, sr = need_gpu()
@@ -162,7 +173,7 @@ def test_memory_planned_run_matches_given_budget():
     assert o["rounds"] == 0 and o["generated_tokens"] == c.n * c.max_new_tokens
 
 
-@pytest.mark.parametrize("name", ["small_bf16"])
+@pytest.mark.parametrize("name", ["small_bf16", "hd128_bf16"])
 def test_bf16_audit(name):
     torch, sr = need_gpu()
     say(f"{name} e2e audit")
