@@ -96,7 +96,7 @@ def test_tiny_fp32_matches_full_oracle(over):
 
 
 @pytest.mark.parametrize("name,over,rtol", [("tiny_fp32", {}, 1e-5), ("tiny_fp32", {"eos_id": 2}, 1e-5),
-                                             ("small_bf16", {}, 2e-2)])
+                                             ("small_bf16", {}, 2e-2), ("hd128_bf16", {}, 2e-2)])
 def test_reward_cache_matches_recompute(name, over, rtol):
     """Scoring through the reward model's cached K/V of the survivors and
     re-running whole responses give the same first-round scores bit for bit
