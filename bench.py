@@ -100,7 +100,7 @@ def main():
     ap.add_argument("--config", default="8b_bf16")
     ap.add_argument("--alpha", type=float, default=None)
     ap.add_argument("--tau", type=int, default=None)
-    ap.add_argument("--profile-every", type=int, default=16)
+    ap.add_argument("--profile-every", type=int, default=64)
     ap.add_argument("--no-bon", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=8)

@@ -299,42 +299,62 @@ struct Model {
 struct Profiler {
   hipStream_t s = nullptr;
   bool active = false;
-  std::vector<hipEvent_t> pool;
+  // Launches are recorded in batches that alternate between two event
+  // pools: `recs` (pool[cur]) is being recorded, `prev` (pool[cur ^ 1]) is
+  // the batch before it.
+  std::vector<hipEvent_t> pool[2];
+  int cur = 0;
   size_t used = 0;
   struct Rec {
     int cls;
     size_t e0, e1;
     double bytes, flops;
   };
-  std::vector<Rec> recs;
+  std::vector<Rec> recs, prev;
   double sec[SR_K_NCLASS] = {}, bytes[SR_K_NCLASS] = {}, flops[SR_K_NCLASS] = {};
   int64_t n[SR_K_NCLASS] = {};
   ~Profiler() {
-    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+    for (auto& p : pool)
+      for (hipEvent_t e : p) (void)hipEventDestroy(e);
   }
   size_t mark() {
-    if (used == pool.size()) {
+    std::vector<hipEvent_t>& p = pool[cur];
+    if (used == p.size()) {
       hipEvent_t e;
       SR_HIP(hipEventCreate(&e));
-      pool.push_back(e);
+      p.push_back(e);
     }
-    SR_HIP(hipEventRecord(pool[used], s));
+    SR_HIP(hipEventRecord(p[used], s));
     return used++;
   }
-  // Waits for the recorded launches and accumulates their durations.
-  void flush() {
-    if (!recs.empty()) {
-      SR_HIP(hipEventSynchronize(pool[recs.back().e1]));
-      for (const Rec& r : recs) {
-        float ms = 0.f;
-        SR_HIP(hipEventElapsedTime(&ms, pool[r.e0], pool[r.e1]));
-        sec[r.cls] += ms * 1e-3;
-        bytes[r.cls] += r.bytes;
-        flops[r.cls] += r.flops;
-        n[r.cls] += 1;
-      }
-      recs.clear();
+  // Waits for the launches of batch v (events of pool p) and accumulates
+  // their durations.
+  void drain(std::vector<Rec>& v, std::vector<hipEvent_t>& p) {
+    if (v.empty()) return;
+    SR_HIP(hipEventSynchronize(p[v.back().e1]));
+    for (const Rec& r : v) {
+      float ms = 0.f;
+      SR_HIP(hipEventElapsedTime(&ms, p[r.e0], p[r.e1]));
+      sec[r.cls] += ms * 1e-3;
+      bytes[r.cls] += r.bytes;
+      flops[r.cls] += r.flops;
+      n[r.cls] += 1;
     }
+    v.clear();
+  }
+  // After a profiled decode step: accumulate the batch before it (long
+  // complete) and start a new batch, so the stream is not drained for the
+  // profiler.
+  void rotate() {
+    drain(prev, pool[cur ^ 1]);
+    prev.swap(recs);
+    cur ^= 1;
+    used = 0;
+  }
+  // Waits for every recorded launch and accumulates it.
+  void flush() {
+    drain(prev, pool[cur ^ 1]);
+    drain(recs, pool[cur]);
     used = 0;
   }
 };
@@ -701,7 +721,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
         timed(c, SR_K_SAMPLE, (double)b * gd.V * 4, 0.0, [&] {
           logprob_accumulate(L.logits, sa.row_stride, b, gd.V, st.cand, st.tok, st.len, step, L.lp_sum, s);
         });
-      if (prof.active) prof.flush();
+      if (prof.active) prof.rotate();
     }
     prof.active = every > 0;
     out->sec_decode += tph.stop();
