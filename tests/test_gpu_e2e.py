@@ -234,3 +234,29 @@ def test_tiny_fp32_logprob_reward_matches_full_oracle(over):
         assert sorted(k for k, a in zip(cand, acc) if a) == sorted(racc)
     assert out["best_index"] == ref["best"] and out["tokens"] == ref["tokens"]
     assert abs(out["best_score"] - ref["score"]) <= 1e-4 * max(1.0, abs(ref["score"]))
+
+
+def test_profiled_run_matches_unprofiled():
+    """Event timing of the launches (profile_every > 0) changes no result,
+    times every launch of the profiled decode steps (one decode-attention
+    record per layer and step) plus every reward and cut launch, and reads
+    its event batches back without loss."""
+    torch, sr = need_gpu()
+    c, gen, rm, prompt = device_models("hd128_bf16")
+    say("hd128_bf16 profiled vs unprofiled")
+    runs = []
+    for every in (0, 3):
+        p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id,
+                           c.max_rounds, profile_every=every)
+        runs.append(sr.generate(gen, rm, prompt, p))
+    a, b = runs
+    assert a["tokens"] == b["tokens"]
+    assert a["best_index"] == b["best_index"] and a["best_score"] == b["best_score"]
+    assert all(k["launches"] == 0 for k in a["kernels"].values())
+    kb = b["kernels"]
+    profiled_steps = [s for s in range(1, c.max_new_tokens) if s % 3 == 0]
+    assert kb["decode_attn"]["launches"] == c.model.n_layers * len(profiled_steps)
+    # (300 rows and fewer: every decode projection is in the weight-bound class)
+    assert kb["gen_gemm_mfma"]["launches"] == 0
+    for name in ("gen_gemm_hbm", "decode_attn", "rm_gemm", "prefill_attn", "sample", "cut"):
+        assert kb[name]["launches"] > 0 and kb[name]["sec"] > 0 and kb[name]["bytes"] > 0, name
