@@ -985,8 +985,9 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   for (int t = 0; t < nk; ++t) {
     // step t landed; every wave is done with step t - 1's buffer
     constexpr int VMN = (NST - 2) * D;
-    static_assert(VMN >= 0 && VMN <= 48 && VMN % 2 == 0, "wait count");
+    static_assert(VMN >= 0 && VMN <= 48, "wait count");
     if constexpr (VMN == 0) SR_VMB(0);
+    else if constexpr (VMN == 11) SR_VMB(11);
     else if constexpr (VMN == 2) SR_VMB(2);
     else if constexpr (VMN == 4) SR_VMB(4);
     else if constexpr (VMN == 6) SR_VMB(6);
@@ -1359,7 +1360,7 @@ static int stream_max_rows() {
   return v;
 }
 
-static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : 128); }
+static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : (M <= 112 ? 112 : 128)); }
 
 // Tiles of 256 x 256 from which a few hundred rows take that tile with the
 // three-deep weight ring instead of the 256 x 128 tile (0: never).
@@ -1588,6 +1589,11 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     } else if (plan.stream == 64) {
       if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true);
       else SR_STREAM(64, 64, 2, 2, 4, false);
+    } else if (plan.stream == 112) {
+      // 65-112 rows: seven 16-row blocks per wave, the four waves side by
+      // side over the columns (less padding than 128 rows)
+      if (g.paired) SR_STREAM(112, 64, 1, 4, 2, true);
+      else SR_STREAM(112, 64, 1, 4, 3, false);
     } else {
       if (g.paired) SR_STREAM(128, 64, 2, 2, 2, true);
       else SR_STREAM(128, 64, 2, 2, 3, false);
