@@ -473,8 +473,7 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
 }
 
 template <typename T, int HD>
-__global__ void decode_merge_kernel(const float* __restrict__ part, int splits, int hq,
-                                    T* __restrict__ out) {
+__global__ void decode_merge_kernel(const float* __restrict__ part, int splits, T* __restrict__ out) {
   const int rq = blockIdx.x;  // row * hq + qh
   const float* p = part + (int64_t)rq * splits * (HD + 2);
   float M = -INFINITY;
@@ -606,7 +605,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     if (pre) {
       prefix_pass(tsplits);
     } else if (!direct) {
-      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, tsplits, a.hq,
+      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, tsplits,
                          (T*)a.out);
       SR_CHECK_LAUNCH();
     }
@@ -641,7 +640,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   SR_CHECK_LAUNCH();
   if (splits > 1) {
     hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part,
-                       splits, a.hq, (T*)a.out);
+                       splits, (T*)a.out);
     SR_CHECK_LAUNCH();
   }
 }
