@@ -107,3 +107,44 @@ def test_teacher_forced_many_rows_head_dim_128():
     for r in (0, 131, rows - 1):
         refl = og.logits(list(prompt) + list(toks[r]))[len(prompt) - 1: len(prompt) - 1 + length]
         assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max(), r
+
+
+def test_8b_layer_shapes_at_run_row_counts():
+    """The 8B shape's layers (d 4096, 32 query / 8 KV heads of 128, ffn
+    14336, vocab 128256, RoPE theta 5e5, prompt 256) with two of them, so the
+    float64 oracle stays quick, at the row counts of the 8B run's rounds:
+    512 rows (256 x 256 and 256 x 128 projection tiles, 32-key streaming
+    attention with the batched prefix pass, fused QKV finalize), 103 rows
+    (112-row streaming tiles, 32-key streaming attention over prefix and
+    tail) and a reward-model prefill of 1536 tokens (256 x 256 tiles).
+    Sampled rows against the oracle."""
+    import synth
+    from oracle.transformer import Transformer
+    torch, sr = need_gpu()
+    shape = synth.ModelShape(2, 4096, 32, 8, 128, 14336, 128256, "bf16", 500000.0)
+    say(f"8B layer shapes {shape}")
+    gw, rw = synth.model_weights(shape, 0, False), synth.model_weights(shape, 1, True)
+    gen, rm = sr.DeviceModel.upload(shape, gw, False), sr.DeviceModel.upload(shape, rw, True)
+    prompt = synth.tokens(256, shape.vocab, 5)
+    rng = np.random.default_rng(8)
+    length = 3
+    og = Transformer(shape, gw, False)
+    for rows in (512, 103):
+        toks = rng.integers(0, shape.vocab, size=(rows, length)).astype(np.int32)
+        p = sr.make_params(rows, 0.8, length, length)
+        ws = sr.Workspace(gen, rm, len(prompt), p)
+        lg = sr.logits_teacher_forced(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), ws).cpu().numpy()
+        for r in (0, rows // 2, rows - 1):
+            refl = og.logits(list(prompt) + list(toks[r]))[len(prompt) - 1: len(prompt) - 1 + length]
+            assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max(), (rows, r)
+        if rows == 512:
+            lens = np.full(rows, length, dtype=np.int32)
+            lens[1::2] = 2
+            got = sr.reward_scores(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(),
+                                   ws).cpu().numpy()
+            orm = Transformer(shape, rw, True)
+            for r in (0, 1, rows - 1):
+                ref = orm.score(list(prompt) + list(toks[r, :lens[r]]))
+                assert abs(got[r] - ref) <= 2e-2 * max(abs(ref), np.abs(got).max()), (r, got[r], ref)
+            del orm
+        del ws
