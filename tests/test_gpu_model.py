@@ -116,8 +116,9 @@ def test_8b_layer_shapes_at_run_row_counts():
     512 rows (256 x 256 and 256 x 128 projection tiles, 32-key streaming
     attention with the batched prefix pass, fused QKV finalize), 103 rows
     (112-row streaming tiles, 32-key streaming attention over prefix and
-    tail) and a reward-model prefill of 1536 tokens (256 x 256 tiles).
-    Sampled rows against the oracle."""
+    tail), 21 rows (32-row streaming tiles, 64-key attention split and
+    merged) and the first cut's reward-model prefill of 512 x 128 tokens
+    (256 x 256 tiles).  Sampled rows against the oracle."""
     import synth
     from oracle.transformer import Transformer
     torch, sr = need_gpu()
@@ -129,7 +130,7 @@ def test_8b_layer_shapes_at_run_row_counts():
     rng = np.random.default_rng(8)
     length = 3
     og = Transformer(shape, gw, False)
-    for rows in (512, 103):
+    for rows in (512, 103, 21):
         toks = rng.integers(0, shape.vocab, size=(rows, length)).astype(np.int32)
         p = sr.make_params(rows, 0.8, length, length)
         ws = sr.Workspace(gen, rm, len(prompt), p)
@@ -137,14 +138,18 @@ def test_8b_layer_shapes_at_run_row_counts():
         for r in (0, rows // 2, rows - 1):
             refl = og.logits(list(prompt) + list(toks[r]))[len(prompt) - 1: len(prompt) - 1 + length]
             assert np.abs(lg[r] - refl).max() <= 2e-2 * np.abs(refl).max(), (rows, r)
-        if rows == 512:
-            lens = np.full(rows, length, dtype=np.int32)
-            lens[1::2] = 2
-            got = sr.reward_scores(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(),
-                                   ws).cpu().numpy()
-            orm = Transformer(shape, rw, True)
-            for r in (0, 1, rows - 1):
-                ref = orm.score(list(prompt) + list(toks[r, :lens[r]]))
-                assert abs(got[r] - ref) <= 2e-2 * max(abs(ref), np.abs(got).max()), (r, got[r], ref)
-            del orm
         del ws
+    # the first cut's reward-model prefill: 512 responses of 128 tokens
+    # (65 536 tokens, as in the 8B run), a few rows of ragged length
+    rows, rl = 512, 128
+    toks = rng.integers(0, shape.vocab, size=(rows, rl)).astype(np.int32)
+    lens = np.full(rows, rl, dtype=np.int32)
+    lens[1], lens[rows - 2] = 77, 1
+    p = sr.make_params(rows, 0.8, rl, rl)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    got = sr.reward_scores(gen, rm, prompt, p, torch.from_numpy(toks).cuda(), torch.from_numpy(lens).cuda(),
+                           ws).cpu().numpy()
+    orm = Transformer(shape, rw, True)
+    for r in (0, 1, rows - 2, rows - 1):
+        ref = orm.score(list(prompt) + list(toks[r, :lens[r]]))
+        assert abs(got[r] - ref) <= 2e-2 * max(abs(ref), np.abs(got).max()), (r, got[r], ref)
