@@ -12,6 +12,12 @@
     python3 <repo>/paper_2410_20290_amd/probes.py attn
         Timing of decode attention at the row counts and tail lengths of the
         three rounds of the 8B-shaped run.
+    python3 <repo>/paper_2410_20290_amd/probes.py vendor [rows]
+        For comparison only: the four projections of the 8B-shaped model at
+        one row count (default 32768, a reward-model prefill chunk) through
+        sr_projection and through torch.matmul (the vendor GEMM library) on
+        the same operands; the library's product is plain (no SwiGLU, bf16
+        out), so it writes more bytes than the fused paired projection.
 """
 import json
 import os
@@ -150,6 +156,33 @@ def attn(cases):
         print(json.dumps({"rows": rows, "lt": lt, "us": round(t * 1e6, 1), "GBs": round(by / t / 1e9)}), flush=True)
 
 
+def vendor(M):
+    import torch
+
+    def etime(f, reps=10):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    for name, N, K, mode in SHAPES[:4]:
+        x, w, out, part, need, nw = _operands(torch, M, N, K, mode)
+        t_sr = etime(lambda: _launch(torch, x, w, out, part, need, M, N, K, mode))
+        xb, wb = x.view(torch.bfloat16), w.view(torch.bfloat16)
+        t_lib = etime(lambda: torch.matmul(xb, wb.t()))
+        fl = 2.0 * M * nw * K
+        print(json.dumps({"M": M, "op": name, "sr_us": round(t_sr * 1e6, 1), "sr_TFLOPs": round(fl / t_sr / 1e12),
+                          "library_us": round(t_lib * 1e6, 1), "library_TFLOPs": round(fl / t_lib / 1e12)}),
+              flush=True)
+        del x, w, out, part, xb, wb
+        torch.cuda.empty_cache()
+
+
 def sample_timing(rows_list):
     """Graph-replay timing of the sampler over 8B-shaped logits rows."""
     import torch
@@ -187,6 +220,8 @@ if __name__ == "__main__":
         traffic()
     elif sys.argv[1] == "sample":
         sample_timing([512, 103, 21])
+    elif sys.argv[1] == "vendor":
+        vendor(int(sys.argv[2]) if len(sys.argv) > 2 else 32768)
     elif sys.argv[1] == "attn":
         attn([(512, 64), (512, 128), (103, 200), (103, 400), (103, 630), (21, 650), (21, 850), (21, 1020)])
     else:

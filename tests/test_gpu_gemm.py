@@ -21,7 +21,9 @@ SHAPES = [(1, 64, 64), (17, 100, 128), (33, 1000, 512), (100, 384, 4096), (129, 
           # a few hundred rows with enough 256 x 256 tiles for the three-deep weight ring
           (300, 49152, 256), (257, 24576, 128),
           # the 103-row QKV projection of the 8B shape (48-column streaming tiles)
-          (103, 6144, 4096)]
+          (103, 6144, 4096),
+          # thousands of rows, ragged in M and N, ten K steps (the 256 x 256 tile)
+          (2600, 1100, 640)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
