@@ -492,8 +492,9 @@ gemm_big_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // rotate from step to step), so the buffer is free after quarter 1: the
 // DMAs of the step after next are spread over quarters 2 and 3 (A rows, then
 // B rows), which keeps the vector-memory path from backing up into the MFMA
-// issue.  Two barriers per step: after quarter 1 (buffer read by all waves)
-// and after quarter 2 (next step landed in all waves).  LDS rows hold eight
+// issue.  One barrier per step, after quarter 1: the buffer has been read by
+// all waves and the next step (whose DMAs went out under quarters 2 and 3 of
+// the step before) has landed in all of them.  LDS rows hold eight
 // 16-byte chunks; chunk c of tile row r sits in slot c ^ (r & 7) ^ ((r >> 3) & 3)
 // (a function of r mod 32, so fragment blocks of 32 rows share it), which puts the fragment reads of any 8 or 16 consecutive rows on distinct
 // banks.
@@ -647,7 +648,11 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
   read_frags(0, 0, 0, a0, b0);
   // One K step with its quarter 0 in (xa, xb); quarter 3 reuses those
   // registers and the next step's quarter 0 goes to (ya, yb).  bb, bbn: B
-  // ring slots of steps t and t + 1.
+  // ring slots of steps t and t + 1.  One barrier per step, after quarter 1:
+  // every wave has read the buffers of step t, and step t + 1 has landed
+  // (all but this wave's newest DMAs: none with two stages, the B rows of
+  // step t + 2 with three).  Then the A rows of step t + 2 go out under
+  // quarter 2 and the B rows of step t + BRING under quarter 3.
   auto step = [&](int t, int bb, int bbn, bf16x8(&xa)[4], bf16x8(&xb)[4], bf16x8(&ya)[4], bf16x8(&yb)[4],
                   bf16x8(&za)[4], bf16x8(&zb)[4]) {
     const int buf = t & 1;
@@ -659,22 +664,17 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     read_frags(buf, bb, 3, xa, xb);
     mfma(ya, yb);
     reads8();
-    // every wave has read all of buffer `buf`
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if constexpr (BRING == 3) SR_VM_BARRIER(8);
+    else SR_VM_BARRIER(0);
     __builtin_amdgcn_sched_barrier(0);
     issue_half(nx, buf, 0);
-    mfma(za, zb);
-    dma8();
-    // step t + 1 landed: all but this wave's newest DMAs (the A rows just
-    // issued; with BRING = 3 also the B rows of step t + 2), in every wave
-    if constexpr (BRING == 3) SR_VM_BARRIER(16);
-    else SR_VM_BARRIER(8);
-    __builtin_amdgcn_sched_barrier(0);
     // (after the last step this reads a stale buffer that is never used)
     read_frags(buf ^ 1, bbn, 0, ya, yb);
+    mfma(za, zb);
+    reads8_dma8();
     issue_half(nxb, bb, 1);
     mfma(xa, xb);
-    reads8_dma8();
+    dma8();
   };
   for (int t = 0; t < nk; t += 3) {
     // B ring slots: t % 3 with three (t is a multiple of 3 here), t % 2 with two
