@@ -65,6 +65,21 @@ __device__ __forceinline__ void dma16(const char* src, bf16_t* lds_dst) {
   __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
 }
 
+// The same copy as a buffer load into LDS (buffer_load_dwordx4 ... lds): the
+// source is base + voff + soff, with the base in a buffer resource (SGPRs),
+// a 32-bit per-lane offset and a wave-uniform scalar offset, so no 64-bit
+// address arithmetic per copy.  The resource is raw (no stride) with the
+// largest record count, so no offset below 4 GiB is range-checked away;
+// 0x00020000 is the gfx9-family word 3 (32-bit data format).
+typedef __amdgpu_buffer_rsrc_t BufRsrc;
+__device__ __forceinline__ BufRsrc buf_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, 0x00020000);
+}
+__device__ __forceinline__ void dma16(BufRsrc r, uint32_t voff, int soff, bf16_t* lds_dst) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds_dst, 16, (int)voff,
+                                           soff, 0, 0);
+}
+
 // ---- wavefront reductions (64 lanes) ---------------------------------------
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
