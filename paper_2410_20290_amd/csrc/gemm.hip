@@ -1500,12 +1500,14 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   return p;
 }
 
-// The LDS-DMA kernel addresses its operands with 32-bit byte offsets from the
-// K base of the split.
-static bool dma_offsets_fit(const GemmArgs& g) {
+// The LDS-DMA kernels address their operands with 32-bit byte offsets from
+// the K base of the split; the tiled ones pass them to buffer loads as signed
+// 32-bit vector offsets, so there they stay below 2 GiB (larger operands take
+// the register-staged kernels).
+static bool dma_offsets_fit(const GemmArgs& g, int bits = 32) {
   const int64_t a = ((int64_t)(g.M - 1) * g.lda + g.K) * 2;
   const int64_t b = ((g.paired ? g.pair_off : 0) + (int64_t)(g.N - 1) * g.ldb + g.K) * 2;
-  return a < (1LL << 32) && b < (1LL << 32) && g.pair_off >= 0;
+  return a < (1LL << bits) && b < (1LL << bits) && g.pair_off >= 0;
 }
 
 int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
@@ -1598,7 +1600,7 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     }
 #undef SR_STREAM
     SR_CHECK_LAUNCH();
-  } else if (plan.dma3 && dma_offsets_fit(g)) {
+  } else if (plan.dma3 && dma_offsets_fit(g, 31)) {
     const int bn_out = g.paired ? 64 : 128;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
     if (g.paired)
@@ -1608,7 +1610,7 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
       hipLaunchKernelGGL(gemm_dma3_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
                          (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     SR_CHECK_LAUNCH();
-  } else if (plan.dma && dma_offsets_fit(g)) {
+  } else if (plan.dma && dma_offsets_fit(g, 31)) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
 #define SR_DMA(P, R)                                                                                   \
