@@ -701,8 +701,8 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
 // free from its start, so the 12 DMA instructions per wave of the step after
 // next are spread over quarter steps 0-2 and the data of step t + 1 has a
 // whole step to land; one barrier per step, before quarter 3.  4 waves, each
-// a 128 x 64 tile of 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators; LDS rows
-// and their swizzle as in the 256 x 256 kernel.
+// a 128 x 64 tile of 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators; LDS rows,
+// their swizzle and the buffer-load copies as in the 256 x 256 kernel.
 #define SR_VMB3(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
 template <bool PAIRED>
