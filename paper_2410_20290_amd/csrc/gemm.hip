@@ -855,6 +855,37 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
 }
 #undef SR_VMB3
 
+// s_waitcnt vmcnt(N) lgkmcnt(0) then s_barrier, N a compile-time count; and
+// the same with N = A * D for a run-time a <= A (copies of a later stages of
+// D instructions each may stay in flight).
+template <int N>
+__device__ __forceinline__ void vm_barrier() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+#define SR_VMB_CASE(n) \
+  if constexpr (N == n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  SR_VMB_CASE(0) SR_VMB_CASE(1) SR_VMB_CASE(2) SR_VMB_CASE(3) SR_VMB_CASE(4) SR_VMB_CASE(5) SR_VMB_CASE(6)
+  SR_VMB_CASE(7) SR_VMB_CASE(8) SR_VMB_CASE(9) SR_VMB_CASE(10) SR_VMB_CASE(11) SR_VMB_CASE(12)
+  SR_VMB_CASE(13) SR_VMB_CASE(14) SR_VMB_CASE(15) SR_VMB_CASE(16) SR_VMB_CASE(17) SR_VMB_CASE(18)
+  SR_VMB_CASE(19) SR_VMB_CASE(20) SR_VMB_CASE(21) SR_VMB_CASE(22) SR_VMB_CASE(23) SR_VMB_CASE(24)
+  SR_VMB_CASE(25) SR_VMB_CASE(26) SR_VMB_CASE(27) SR_VMB_CASE(28) SR_VMB_CASE(29) SR_VMB_CASE(30)
+  SR_VMB_CASE(31) SR_VMB_CASE(32) SR_VMB_CASE(33) SR_VMB_CASE(34) SR_VMB_CASE(35) SR_VMB_CASE(36)
+  SR_VMB_CASE(37) SR_VMB_CASE(38) SR_VMB_CASE(39) SR_VMB_CASE(40) SR_VMB_CASE(41) SR_VMB_CASE(42)
+  SR_VMB_CASE(43) SR_VMB_CASE(44) SR_VMB_CASE(45) SR_VMB_CASE(46) SR_VMB_CASE(47) SR_VMB_CASE(48)
+  SR_VMB_CASE(49) SR_VMB_CASE(50) SR_VMB_CASE(51) SR_VMB_CASE(52) SR_VMB_CASE(53) SR_VMB_CASE(54)
+  SR_VMB_CASE(55) SR_VMB_CASE(56) SR_VMB_CASE(57) SR_VMB_CASE(58) SR_VMB_CASE(59) SR_VMB_CASE(60)
+  SR_VMB_CASE(61) SR_VMB_CASE(62) SR_VMB_CASE(63)
+#undef SR_VMB_CASE
+}
+template <int D, int A>
+__device__ __forceinline__ void vm_barrier_ahead(int a) {
+  if constexpr (A <= 0) {
+    vm_barrier<0>();
+  } else {
+    if (a >= A) vm_barrier<A * D>();
+    else vm_barrier_ahead<D, A - 1>(a);
+  }
+}
+
 // ------------------------------------- bf16 MFMA GEMM, few rows (LDS DMA)
 // For the decode projections (a few hundred rows at most) the weights are
 // streamed once from HBM; what matters is keeping enough of them in flight
@@ -868,7 +899,6 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
 // grid, each a (BM / WGM) x (BN / WGN) tile of v_mfma_f32_16x16x32_bf16
 // accumulators; the fragment reads of the next 32-wide sub-step run under
 // the MFMAs of the current one.
-#define SR_VMB(n) asm volatile("s_waitcnt vmcnt(" #n ") lgkmcnt(0)\n\ts_barrier" ::: "memory")
 
 template <int BK>
 __device__ __forceinline__ int stream_slot(int c, int r) {
@@ -979,36 +1009,15 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  for (int st = 0; st < NST - 1; ++st) issue(min(st, nk - 1), st);
+  // Only steps that exist are fetched (a copy past the end would be waited
+  // for before the work-group may end, a DMA round trip on every launch).
+  for (int st = 0; st < NST - 1 && st < nk; ++st) issue(st, st);
   for (int t = 0; t < nk; ++t) {
-    // step t landed; every wave is done with step t - 1's buffer
-    constexpr int VMN = (NST - 2) * D;
-    static_assert(VMN >= 0 && VMN <= 48, "wait count");
-    if constexpr (VMN == 0) SR_VMB(0);
-    else if constexpr (VMN == 11) SR_VMB(11);
-    else if constexpr (VMN == 2) SR_VMB(2);
-    else if constexpr (VMN == 4) SR_VMB(4);
-    else if constexpr (VMN == 6) SR_VMB(6);
-    else if constexpr (VMN == 8) SR_VMB(8);
-    else if constexpr (VMN == 10) SR_VMB(10);
-    else if constexpr (VMN == 12) SR_VMB(12);
-    else if constexpr (VMN == 14) SR_VMB(14);
-    else if constexpr (VMN == 16) SR_VMB(16);
-    else if constexpr (VMN == 18) SR_VMB(18);
-    else if constexpr (VMN == 20) SR_VMB(20);
-    else if constexpr (VMN == 22) SR_VMB(22);
-    else if constexpr (VMN == 24) SR_VMB(24);
-    else if constexpr (VMN == 26) SR_VMB(26);
-    else if constexpr (VMN == 28) SR_VMB(28);
-    else if constexpr (VMN == 30) SR_VMB(30);
-    else if constexpr (VMN == 32) SR_VMB(32);
-    else if constexpr (VMN == 36) SR_VMB(36);
-    else if constexpr (VMN == 40) SR_VMB(40);
-    else if constexpr (VMN == 42) SR_VMB(42);
-    else if constexpr (VMN == 44) SR_VMB(44);
-    else if constexpr (VMN == 48) SR_VMB(48);
-    else static_assert(VMN < 0, "add this wait count");
-    issue(min(t + NST - 1, nk - 1), (t + NST - 1) % NST);
+    // step t landed; every wave is done with step t - 1's buffer: all but
+    // the copies of the steps issued after t (NST - 2 of them, fewer at the
+    // end).
+    vm_barrier_ahead<D, NST - 2>(min(NST - 2, nk - 1 - t));
+    if (t + NST - 1 < nk) issue(t + NST - 1, (t + NST - 1) % NST);
     const bf16_t* base = lds + (t % NST) * STAGE;
     bf16x8 a0[TI], b0[NB][TJ], a1[TI], b1[NB][TJ];
     read_frags(base, 0, a0, b0);
@@ -1085,7 +1094,6 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     }
   }
 }
-#undef SR_VMB
 
 // -------------------------------------------- bf16 MFMA GEMM, few rows
 // For M <= 128 (decode after the cuts) the weights dominate: every weight
