@@ -9,6 +9,7 @@
 // Split-K writes fp32 partials [split][M][Nout] that a consumer sums in
 // split order, so results do not depend on scheduling.
 #include <cstdlib>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -796,7 +797,7 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     __builtin_amdgcn_sched_barrier(0);
   };
-  // quarter 3: (MFMA, read) x 6, then 2 MFMAs
+  // quarter 3 (and quarters 0-2 of the last two steps): (MFMA, read) x 6, then 2 MFMAs
   auto reads = [] {
 #pragma unroll
     for (int q = 0; q < 6; ++q) {
@@ -817,33 +818,56 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): no scalar loads in flight past here
   bf16x8 a0[4], b0[2], a1[4], b1[2];
   read_frags(0, 0, a0, b0);
-  for (int t = 0; t < nk; ++t) {
+  // One step; `live`: the step after next exists and is fetched (the last
+  // two steps fetch nothing and wait for every copy, so no copy is in flight
+  // at the end).
+  auto step = [&](auto live, int t) {
+    constexpr bool FETCH = decltype(live)::value;
     const int buf = t % 3, nb = (t + 1) % 3, wb = (t + 2) % 3;
-    const int nx = min(t + 2, nk - 1);
+    const int nx = t + 2;
     read_frags(buf, 1, a1, b1);
+    if constexpr (FETCH) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma(nx, wb, i);
-    mfma(a0, b0);
-    reads_dmas();
+      for (int i = 0; i < 4; ++i) dma(nx, wb, i);
+      mfma(a0, b0);
+      reads_dmas();
+    } else {
+      mfma(a0, b0);
+      reads();
+    }
     read_frags(buf, 2, a0, b0);
+    if constexpr (FETCH) {
 #pragma unroll
-    for (int i = 4; i < 8; ++i) dma(nx, wb, i);
-    mfma(a1, b1);
-    reads_dmas();
+      for (int i = 4; i < 8; ++i) dma(nx, wb, i);
+      mfma(a1, b1);
+      reads_dmas();
+    } else {
+      mfma(a1, b1);
+      reads();
+    }
     read_frags(buf, 3, a1, b1);
+    if constexpr (FETCH) {
 #pragma unroll
-    for (int i = 8; i < 12; ++i) dma(nx, wb, i);
-    mfma(a0, b0);
-    reads_dmas();
-    // step t + 1 landed (all but this wave's 12 newest DMAs) in every wave,
-    // and every wave has read all it needs of buffer `buf`
-    SR_VMB3(12);
+      for (int i = 8; i < 12; ++i) dma(nx, wb, i);
+      mfma(a0, b0);
+      reads_dmas();
+      // step t + 1 landed (all but this wave's 12 newest DMAs) in every
+      // wave, and every wave has read all it needs of buffer `buf`
+      SR_VMB3(12);
+    } else {
+      mfma(a0, b0);
+      reads();
+      SR_VMB3(0);
+    }
     __builtin_amdgcn_sched_barrier(0);
     // (after the last step this reads a stale buffer that is never used)
     read_frags(nb, 0, a0, b0);
     mfma(a1, b1);
     reads();
-  }
+  };
+  int t = 0;
+  for (; t < nk - 2; ++t) step(std::true_type{}, t);
+  for (; t < nk; ++t) step(std::false_type{}, t);
   // no DMA may still be writing LDS and no wave still reading it
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   float* st = reinterpret_cast<float*>(lds) + wave * 8192;
