@@ -69,7 +69,8 @@ __device__ __forceinline__ void dma16(const char* src, bf16_t* lds_dst) {
 // source is base + voff + soff, with the base in a buffer resource (SGPRs),
 // a 32-bit per-lane offset and a wave-uniform scalar offset, so no 64-bit
 // address arithmetic per copy.  The resource is raw (no stride) with the
-// largest record count, so no offset below 4 GiB is range-checked away;
+// largest record count, so no offset is range-checked away; the vector
+// offset goes in as a signed int, so callers keep it below 2 GiB.
 // 0x00020000 is the gfx9-family word 3 (32-bit data format).
 typedef __amdgpu_buffer_rsrc_t BufRsrc;
 __device__ __forceinline__ BufRsrc buf_rsrc(const void* base) {
