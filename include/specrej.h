@@ -174,7 +174,19 @@ typedef struct {
  *  all_tokens, all_len           [n][max_new_tokens], [n] every candidate's
  *                                response as far as it was generated.
  *  final_scores                  [n] reward of completed candidates (members
- *                                of the set I), NaN for rejected ones. */
+ *                                of the set I), NaN for rejected ones.
+ *  watch_cand, n_watch,          the logits rows the run sampled from, for
+ *  watch_logits                  n_watch >= 0 chosen candidates (HOST int32
+ *                                watch_cand[n_watch], each in [0, n)):
+ *                                watch_logits (HOST float
+ *                                [n_watch][max_new_tokens][vocab]) row
+ *                                [w][t] receives the generator's logits from
+ *                                which response token t of candidate
+ *                                watch_cand[w] was drawn, for every t below
+ *                                that candidate's length; rows of later steps
+ *                                hold unspecified values.  Costs one host copy
+ *                                per watched row and step.  n_watch = 0 (or
+ *                                watch_logits NULL) watches nothing. */
 typedef struct {
   int32_t *round_L, *round_b, *round_keep;
   int32_t *round_cand;
@@ -183,6 +195,9 @@ typedef struct {
   int32_t *all_tokens, *all_len;
   float *final_scores;
   int32_t max_rounds_cap;
+  const int32_t *watch_cand;
+  int32_t n_watch;
+  float *watch_logits;
 } sr_trace;
 
 /* Bytes of device workspace sr_generate needs for these models, prompt

@@ -97,5 +97,12 @@ def sample(logits, temperature: float, seed: int, cand: int, step: int) -> int:
     if total == 0:
         return 0
     t = draw_threshold(uniform_word(seed, cand, step), total)
-    cum = np.cumsum(w, dtype=np.uint64)
+    return inverse_cdf(w, t)
+
+
+def inverse_cdf(w, t: int) -> int:
+    """Step 6: the first index i whose cumulative weight w_0 + ... + w_i
+    exceeds t strictly (a t equal to a cumulative weight falls to the next
+    token with positive weight)."""
+    cum = np.cumsum(np.asarray(w, dtype=np.uint64), dtype=np.uint64)
     return int(np.searchsorted(cum, np.uint64(t), side="right"))

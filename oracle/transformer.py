@@ -27,15 +27,37 @@ w2 [nl][d][ff]; bf16 weights as uint16 bit patterns, widened exactly.
 The per-candidate decode state keeps a private KV cache for every row,
 prompt included: nothing is shared between candidates here.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 
-def widen(a) -> np.ndarray:
-    """Weights as float64 (bf16 bit patterns are widened exactly)."""
-    a = np.asarray(a)
+def _widen_block(a) -> np.ndarray:
     if a.dtype == np.uint16:
         return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
     return a.astype(np.float64)
+
+
+def widen(a) -> np.ndarray:
+    """Weights as float64 (bf16 bit patterns are widened exactly).  Large
+    arrays are widened in row blocks on several threads (numpy's casts run
+    without the interpreter lock); the result is the same."""
+    a = np.asarray(a)
+    if a.ndim == 0 or a.size < (1 << 22):
+        return _widen_block(a)
+    out = np.empty(a.shape, dtype=np.float64)
+    flat_in, flat_out = a.reshape(-1), out.reshape(-1)
+    n = flat_in.size
+    parts = min(32, os.cpu_count() or 1)
+    step = -(-n // parts)
+
+    def one(i):
+        flat_out[i * step:(i + 1) * step] = _widen_block(flat_in[i * step:(i + 1) * step])
+
+    with ThreadPoolExecutor(parts) as ex:
+        list(ex.map(one, range(parts)))
+    return out
 
 
 def rmsnorm(x, g, eps):
@@ -154,6 +176,53 @@ class Transformer:
             h = h + o.reshape(T, -1) @ self.w("wo", l).T
             h = h + self._ffn(h, l)
         return rmsnorm(h, self.w("final_norm"), s.rms_eps)
+
+    def forward_many(self, seqs):
+        """``forward`` of several token sequences at once: the final
+        normalised hidden states [T_i][d] of each.  The sequences share each
+        layer's projections (their rows stacked) and attend only to
+        themselves, so every layer's weights are widened once for all of
+        them (for models too large to keep widened)."""
+        s = self.s
+        seqs = [np.asarray(t, dtype=np.int64) for t in seqs]
+        lens = [len(t) for t in seqs]
+        ends = np.cumsum(lens)
+        starts = ends - np.asarray(lens)
+        allt = np.concatenate(seqs)
+        h = self.w("embed")[allt] if self.cache_f64 else widen(self.raw["embed"][allt])
+        pos = np.concatenate([np.arange(T) for T in lens])
+        cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta)
+        cos, sin = cos[:, None, :], sin[:, None, :]
+        for l in range(s.n_layers):
+            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
+            q, k = rope(q, cos, sin), rope(k, cos, sin)
+            o = np.empty_like(q)
+            for b, e in zip(starts, ends):
+                o[b:e] = causal_attention(q[b:e], k[b:e], v[b:e], s.n_kv_heads)
+            h = h + o.reshape(len(allt), -1) @ self.w("wo", l).T
+            h = h + self._ffn(h, l)
+        out = rmsnorm(h, self.w("final_norm"), s.rms_eps)
+        return [out[b:e] for b, e in zip(starts, ends)]
+
+    def logits_at(self, seqs, positions):
+        """Generator logits at chosen positions of several sequences:
+        for sequence i, rows [len(positions[i])][V] with row j the
+        distribution of token positions[i][j] + 1 (as ``logits``)."""
+        assert not self.reward
+        hs = self.forward_many(seqs)
+        head = self.w("head")
+        return [h[np.asarray(p, dtype=np.int64)] @ head.T for h, p in zip(hs, positions)]
+
+    def scores_at(self, seqs, lengths):
+        """Reward-model scores of prefixes: for sequence i and each length L
+        in lengths[i], s(first L tokens) = w_head . out[L - 1].  Under the
+        causal mask the state at position L - 1 depends only on the first L
+        tokens, so one forward over the whole sequence serves every prefix."""
+        assert self.reward
+        hs = self.forward_many(seqs)
+        head = self.w("head")
+        return [np.array([float(h[L - 1] @ head) for L in ls]) for h, ls in zip(hs, lengths)]
 
     def logits(self, tokens):
         """Generator logits [T][V]: row t is the distribution of token t+1."""

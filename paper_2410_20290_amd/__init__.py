@@ -62,7 +62,7 @@ class sr_result(ctypes.Structure):
 class sr_trace(ctypes.Structure):
     _fields_ = [(n, _vp) for n in ("round_L", "round_b", "round_keep", "round_cand", "round_scores",
                                    "round_accept", "all_tokens", "all_len", "final_scores")] + \
-               [("max_rounds_cap", _i32)]
+               [("max_rounds_cap", _i32), ("watch_cand", _vp), ("n_watch", _i32), ("watch_logits", _vp)]
 
 
 _lib = None
@@ -236,8 +236,11 @@ class Workspace:
 
 
 def generate(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, ws: Workspace = None, trace=False,
-             max_rounds_cap=64, stream=None) -> dict:
-    """sr_generate; returns the answer, result summary and (optionally) the trace."""
+             max_rounds_cap=64, stream=None, watch=()) -> dict:
+    """sr_generate; returns the answer, result summary and (optionally) the
+    trace.  ``watch``: candidates whose sampled-from logits rows the trace
+    records (out["trace"]["watch_logits"] [len(watch)][max_new_tokens][vocab];
+    implies trace=True)."""
     prompt = np.ascontiguousarray(np.asarray(prompt, dtype=np.int32))
     if ws is None:
         ws = Workspace(gen, rm, len(prompt), p)
@@ -245,6 +248,8 @@ def generate(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, ws: Worksp
     res = sr_result()
     tr = None
     arrays = {}
+    watch = np.ascontiguousarray(np.asarray(list(watch), dtype=np.int32))
+    trace = trace or len(watch) > 0
     if trace:
         n, R = p.n, max_rounds_cap
         arrays = dict(round_L=np.zeros(R, np.int32), round_b=np.zeros(R, np.int32),
@@ -253,6 +258,10 @@ def generate(gen: DeviceModel, rm: DeviceModel, prompt, p: sr_params, ws: Worksp
                       all_tokens=np.zeros((n, p.max_new_tokens), np.int32), all_len=np.zeros(n, np.int32),
                       final_scores=np.zeros(n, np.float32))
         tr = sr_trace(*[a.ctypes.data for a in arrays.values()], R)
+        if len(watch):
+            wl = np.full((len(watch), p.max_new_tokens, gen.shape.vocab), np.nan, dtype=np.float32)
+            arrays["watch_logits"] = wl
+            tr.watch_cand, tr.n_watch, tr.watch_logits = watch.ctypes.data, len(watch), wl.ctypes.data
     st = lib().sr_generate(ctypes.byref(gen.desc), _mref(rm), prompt.ctypes.data, len(prompt),
                            ctypes.byref(p), ws.ptr, ws.nbytes, _stream(stream), out_tokens.ctypes.data,
                            ctypes.byref(res), ctypes.byref(tr) if tr is not None else None)

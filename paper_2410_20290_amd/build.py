@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libspecrej.so")
 SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "sampler.hip", "cut.hip", "host.cpp", "diagnostics.cpp"]
-ARCH = os.environ.get("SPECREJ_ARCH", "gfx950")
+ARCH = "gfx950"
 COMMON = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", os.path.join(HERE, "..", "include")]

@@ -12,7 +12,6 @@
 // queries of one row and one KV head; K/V tiles are staged in LDS as fp32
 // and shared by all its queries.
 #include <algorithm>
-#include <cstdlib>
 
 #include "common.h"
 #include "kernels.h"
@@ -510,10 +509,7 @@ static int decode_kps(int rows, int hkv, int keys) {
 // grid within one round of resident work-groups (two per CU), at least 64
 // keys per split (a partly filled second round measured slower).
 static int tail_mfma_kps(int rows, int hkv, int keys) {
-  static const int target = [] {
-    const char* e = getenv("SPECREJ_TAIL_WG_TARGET");
-    return e ? atoi(e) : 512;
-  }();
+  constexpr int target = 512;
   const int64_t groups = (int64_t)rows * hkv;
   int splits = (int)std::max<int64_t>(1, target / groups);
   splits = std::max(1, std::min(splits, keys / 64));
@@ -527,16 +523,10 @@ __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16
                                          int hkv, bf16_t* __restrict__ out, float qscale,
                                          float* __restrict__ part, int part_splits);
 
-// Whether the shared prefix is attended by the batched MFMA kernel.
-static int prefix_mfma_min_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_PREFIX_MFMA_MIN_ROWS");
-    return e ? atoi(e) : 128;
-  }();
-  return v;
-}
+// Whether the shared prefix is attended by the batched MFMA kernel (from 128
+// rows; below that it costs more than the L2 reads it saves).
 static bool prefix_by_mfma(int dtype, int hd, int P, int rows) {
-  return dtype == SR_BF16 && hd == 128 && P > 0 && rows >= prefix_mfma_min_rows();
+  return dtype == SR_BF16 && hd == 128 && P > 0 && rows >= 128;
 }
 
 // Partial slots needed for `keys` = prefix + maximal tail (upper bound for
@@ -552,11 +542,7 @@ int decode_attn_splits(int rows, int hkv, int keys) {
 // 16 query heads per KV head, up to 1024 rows: measured faster than the
 // per-query kernel at 21, 103 and 512 rows).
 static bool tail_by_mfma(int dtype, int hd, int g, int rows) {
-  static const int max_rows = [] {
-    const char* e = getenv("SPECREJ_TAIL_MFMA_MAX_ROWS");
-    return e ? atoi(e) : 1024;
-  }();
-  return dtype == SR_BF16 && hd == 128 && g <= 16 && rows <= max_rows;
+  return dtype == SR_BF16 && hd == 128 && g <= 16 && rows <= 1024;
 }
 
 template <int G>

@@ -1119,144 +1119,6 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   }
 }
 
-// -------------------------------------------- bf16 MFMA GEMM, few rows
-// For M <= 128 (decode after the cuts) the weights dominate: every weight
-// element is used by only M rows.  Work-group = 4 waves over 128 output
-// columns (PAIRED: 64 columns, each wave holding gate and up of its 16), all
-// M rows padded to 16 * TM.  The activation chunk (rows x 128 of K) is staged
-// in LDS once and shared by the 4 waves; each wave streams its weight rows
-// straight into registers, two chunks ahead of the MFMAs.
-template <int TM, bool PAIRED>
-__global__ void __launch_bounds__(256)
-gemm_skinny_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
-                   int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
-                   float* __restrict__ partial) {
-  constexpr int KC = 128, AROW = KC + 8, MP = TM * 16;
-  constexpr int COLS = PAIRED ? 64 : 128;
-  constexpr int A_CH = MP * (KC / 8);                 // 16-byte chunks of an A chunk
-  constexpr int A_IT = (A_CH + 255) / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][MP * AROW];
-  const TileIdx tile = tile_of(1, (N + COLS - 1) / COLS, K / k_per_split);
-  if (!tile.valid) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int fr = lane & 15, fg = lane >> 4;
-  const int n0 = tile.n * COLS;
-  const int kb = tile.split * k_per_split;
-  const int nch = k_per_split / KC;
-  // this lane's two weight rows (fragment f = 0, 1)
-  const bf16_t* brow[2];
-  int ncol[2];
-#pragma unroll
-  for (int f = 0; f < 2; ++f) {
-    const int n = PAIRED ? n0 + wave * 16 + fr : n0 + wave * 32 + f * 16 + fr;
-    ncol[f] = n;
-    const int nc = min(n, N - 1);
-    brow[f] = B + ((PAIRED && f == 1) ? pair_off : 0) + (int64_t)nc * ldb + kb + fg * 8;
-  }
-  f32x4 acc[TM][2];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int f = 0; f < 2; ++f) acc[i][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // Weight fragments: a ring of three chunks with static slots (the chunk
-  // loop is unrolled by three), so chunk c + 2 is requested at the top of
-  // iteration c, two chunks of MFMAs ahead of its use.
-  bf16x8 bq0[4][2], bq1[4][2], bq2[4][2];
-  // Loads are unconditional (chunk index and rows clamped, out-of-range rows
-  // zeroed by a select) so that the wait counts stay exact across the loop.
-  auto load_b = [&](int c, bf16x8 (&dst)[4][2]) {
-    const int cc = min(c, nch - 1);
-#pragma unroll
-    for (int st = 0; st < 4; ++st)
-#pragma unroll
-      for (int f = 0; f < 2; ++f)
-        dst[st][f] = *reinterpret_cast<const bf16x8*>(brow[f] + cc * KC + st * 32);
-  };
-  uint4 ra[A_IT];
-  auto load_a = [&](int c) {
-    const int cc = min(c, nch - 1);
-#pragma unroll
-    for (int it = 0; it < A_IT; ++it) {
-      const int ch = min(tid + it * 256, A_CH - 1);
-      const int r = ch / (KC / 8), k8 = ch % (KC / 8);
-      const uint4 v = *reinterpret_cast<const uint4*>(A + (int64_t)min(r, M - 1) * lda + kb + cc * KC + k8 * 8);
-      ra[it] = r < M ? v : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store_a = [&](int buf) {
-#pragma unroll
-    for (int it = 0; it < A_IT; ++it) {
-      const int ch = tid + it * 256;
-      if (ch < A_CH) {
-        const int r = ch / (KC / 8), cc = ch % (KC / 8);
-        *reinterpret_cast<uint4*>(&As[buf][r * AROW + cc * 8]) = ra[it];
-      }
-    }
-  };
-  auto step = [&](int c, bf16x8 (&cur)[4][2], bf16x8 (&ahead)[4][2]) {
-    const int buf = c & 1;
-    load_b(c + 2, ahead);
-    load_a(c + 1);
-    if (c < nch) {
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const bf16x8 af =
-              *reinterpret_cast<const bf16x8*>(&As[buf][(i * 16 + fr) * AROW + st * 32 + fg * 8]);
-#pragma unroll
-          for (int f = 0; f < 2; ++f)
-            acc[i][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, cur[st][f], acc[i][f], 0, 0, 0);
-        }
-      }
-    }
-    store_a(buf ^ 1);
-    __syncthreads();
-  };
-
-  load_b(0, bq0);
-  load_b(1, bq1);
-  load_a(0);
-  store_a(0);
-  __syncthreads();
-  for (int c = 0; c < nch; c += 3) {
-    step(c, bq0, bq2);
-    step(c + 1, bq1, bq0);
-    step(c + 2, bq2, bq1);
-  }
-
-  // lane holds rows 16 i + 4 (lane/16) + e of column fragment f
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int m = i * 16 + fg * 4 + e;
-      if (m >= M) continue;
-      if (PAIRED) {
-        const int n = ncol[0];
-        if (n >= N) continue;
-        if (partial) {
-          float* p = partial + ((int64_t)tile.split * M + m) * (2 * (int64_t)N);
-          p[n] = acc[i][0][e];
-          p[N + n] = acc[i][1][e];
-        } else {
-          store_out(epi, m, n, silu(acc[i][0][e]) * acc[i][1][e]);
-        }
-      } else {
-#pragma unroll
-        for (int f = 0; f < 2; ++f) {
-          const int n = ncol[f];
-          if (n >= N) continue;
-          if (partial)
-            partial[((int64_t)tile.split * M + m) * N + n] = acc[i][f][e];
-          else
-            epi_one(epi, m, n, acc[i][f][e]);
-        }
-      }
-    }
-}
-
 // ------------------------------------------------------------ fp32 GEMM
 // 64 x 64 block tile, 256 threads, 4 x 4 outputs per thread, K step 16.
 // Always writes to `partial` ([1][M][NB*N]); the reduce kernel applies the
@@ -1354,88 +1216,34 @@ size_t gemm_partial_elems_always(int dtype, int M, int N, int K) {
   return (size_t)p.splits * M * (size_t)N;
 }
 
-// Rows from which the 256 x 256 tile is used.
-static int big_tile_min_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_BIG_TILE_MIN_M");
-    return e ? atoi(e) : 1024;
-  }();
-  return v;
-}
-
-static int skinny_max_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_SKINNY_MAX_M");
-    return e ? atoi(e) : 0;
-  }();
-  return v;
-}
-
-// Rows from which the LDS-DMA 256 x 256 tile is used (from 256 rows also
-// when the tile grid alone fills most of the CUs).
-static int dma_min_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_DMA_MIN_M");
-    return e ? atoi(e) : 1024;
-  }();
-  return v;
-}
-
-// Rows up to which the LDS-DMA streaming kernel is used.
-static int stream_max_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_STREAM_MAX_M");
-    return e ? atoi(e) : 128;
-  }();
-  return v;
-}
+// Dispatch thresholds (rows M of the projection), measured on MI355X:
+//  - up to kStreamMaxRows rows the LDS-DMA streaming kernel (weights read
+//    once, one work-group per CU);
+//  - up to kDma3MaxRows rows the 256 x 256 tile with the three-deep weight
+//    ring when its grid holds at least kDmaWideMinTiles tiles, else the
+//    three-stage 256 x 128 tile;
+//  - from kDmaMinRows rows (or 256 rows with kDmaWideMinTiles tiles) the
+//    LDS-DMA 256 x 256 tile, and the register-staged 256 x 256 tile when
+//    an operand is too large for 32-bit buffer offsets.
+constexpr int kStreamMaxRows = 128;
+constexpr int kDma3MaxRows = 512;
+constexpr int kDmaWideMinTiles = 192;
+constexpr int kDmaMinRows = 1024;
+constexpr int kBigTileMinRows = 1024;
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : (M <= 112 ? 112 : 128)); }
-
-// Tiles of 256 x 256 from which a few hundred rows take that tile with the
-// three-deep weight ring instead of the 256 x 128 tile (0: never).
-static int dma_wide_min_tiles() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_DMA_WIDE_MIN_TILES");
-    return e ? atoi(e) : 192;
-  }();
-  return v;
-}
-
-// Rows up to which the three-stage 256 x 128 tile is used (above the
-// streaming kernel's rows).
-static int dma3_max_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_DMA3_MAX_M");
-    return e ? atoi(e) : 512;
-  }();
-  return v;
-}
-
-// Rows below which the 128 x 128 streaming tile (K step 64) takes over from
-// the other tiles for unpaired projections with at most 65536 outputs per
-// row; off by default (it measured even with them end to end).
-static int stream_mid_max_rows() {
-  static int v = [] {
-    const char* e = getenv("SPECREJ_STREAM_MID_MAX_M");
-    return e ? atoi(e) : 0;
-  }();
-  return v;
-}
 
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   GemmPlan p;
   p.splits = 1;
   p.big = false;
-  p.skinny = false;
   p.dma = false;
   p.dma3 = false;
   p.dma_bring = 2;
   p.stream = 0;
   p.stream_bn = 0;
-  p.stream_bk = 128;
   if (dtype != SR_BF16) return p;
-  if (M <= stream_max_rows() && K % 128 == 0 && (M <= 64 || N <= 65536)) {
+  if (M <= kStreamMaxRows && K % 128 == 0 && (M <= 64 || N <= 65536)) {
     // One round of work-groups (one per CU): split K by the largest power of
     // two that keeps the grid within 256 and each split a multiple of 128.
     p.stream = stream_tile_rows(M);
@@ -1446,20 +1254,18 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     p.splits = splits;
     return p;
   }
-  if (M > stream_max_rows() && M <= dma3_max_rows() && K % 64 == 0 && dma_wide_min_tiles() > 0) {
+  if (M > kStreamMaxRows && M <= kDma3MaxRows && K % 64 == 0) {
     // A few hundred rows, a grid of 256 x 256 tiles that alone fills most of
     // the CUs: that tile with the three-deep weight ring, unsplit.
     const int64_t wide = (int64_t)((M + 255) / 256) * ((N + (paired ? 127 : 255)) / (paired ? 128 : 256));
-    if (wide >= dma_wide_min_tiles()) {
+    if (wide >= kDmaWideMinTiles) {
       p.dma = true;
       p.dma_bring = 3;
       return p;
     }
-  }
-  if (M > stream_max_rows() && M <= dma3_max_rows() && K % 64 == 0) {
-    // A few hundred rows (the first decode round): 256 x 128 tiles with
-    // three stages; split K (each split a multiple of 64 and at least 512
-    // long) by powers of two while the grid stays within 256.
+    // Otherwise (the first decode round) 256 x 128 tiles with three stages;
+    // split K (each split a multiple of 64 and at least 512 long) by powers
+    // of two while the grid stays within 256.
     p.dma3 = true;
     const int64_t tiles = (int64_t)((M + 255) / 256) * ((N + (paired ? 63 : 127)) / (paired ? 64 : 128));
     int splits = 1;
@@ -1467,21 +1273,8 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     p.splits = splits;
     return p;
   }
-  if (M > stream_max_rows() && M < stream_mid_max_rows() && K % 64 == 0 && N <= 65536 && !paired) {
-    // A few hundred rows (the first decode round): 128 x 128 tiles with a K
-    // step of 64, split K as above (the paired gate|up projection keeps the
-    // 256 x 256 tile).
-    p.stream = 128;
-    p.stream_bn = paired ? 64 : 128;
-    p.stream_bk = 64;
-    const int64_t tiles = (int64_t)((M + 127) / 128) * ((N + p.stream_bn - 1) / p.stream_bn);
-    int splits = 1;
-    while (tiles * splits * 2 <= 256 && K % (splits * 2 * 64) == 0 && K / (splits * 2) >= 512) splits *= 2;
-    p.splits = splits;
-    return p;
-  }
   const int64_t dma_tiles = (int64_t)((M + 255) / 256) * ((N + (paired ? 127 : 255)) / (paired ? 128 : 256));
-  if (K % 64 == 0 && (M >= dma_min_rows() || (M >= 256 && dma_tiles >= 192))) {
+  if (K % 64 == 0 && (M >= kDmaMinRows || (M >= 256 && dma_tiles >= kDmaWideMinTiles))) {
     // One work-group per CU at least: split K (each split a multiple of 64
     // and at least 512 long) while the tile grid is smaller than 256.
     p.dma = true;
@@ -1492,32 +1285,8 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
     p.splits = splits;
     return p;
   }
-  if (M >= big_tile_min_rows()) {
+  if (M >= kBigTileMinRows) {
     p.big = true;
-    return p;
-  }
-  if (M <= skinny_max_rows() && K % 128 == 0) {
-    // Enough work-groups to fill every CU to its occupancy (fewer rows use
-    // fewer registers and allow more resident work-groups); splits divide K
-    // into multiples of 128.
-    p.skinny = true;
-    const int cols = paired ? 64 : 128;
-    const int64_t tiles = (N + cols - 1) / cols;
-    const int chunks = K / 128;
-    const int tm = (M + 15) / 16;
-    static const int per_cu_env = [] {
-      const char* e = getenv("SPECREJ_SKINNY_WG_PER_CU");
-      return e ? atoi(e) : 0;
-    }();
-    const int per_cu = per_cu_env > 0 ? per_cu_env : (tm <= 2 ? 4 : (tm <= 4 ? 3 : 2));
-    const int64_t target = 256LL * per_cu;
-    int splits = 1;
-    for (int sp = 1; sp <= chunks && sp <= 64; ++sp) {
-      if (chunks % sp) continue;
-      splits = sp;
-      if (tiles * sp >= target) break;
-    }
-    p.splits = splits;
     return p;
   }
   int bm = M <= 32 ? 32 : (M <= 64 ? 64 : 128);
@@ -1572,50 +1341,13 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
                "GEMM partial buffer too small");
     part = partial;
   }
-  if (plan.skinny) {
-    const int cols = g.paired ? 64 : 128;
-    dim3 grid = tile_grid(1, (g.N + cols - 1) / cols, splits);
-    const int tm = (g.M + 15) / 16;
-#define SR_SKINNY(TM)                                                                                \
-  hipLaunchKernelGGL((gemm_skinny_kernel<TM, PAIRED_>), grid, dim3(256), 0, s, (const bf16_t*)g.A, \
-                     g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part)
-#define SR_SKINNY_ALL()                                   \
-  switch (tm) {                                           \
-    case 1: SR_SKINNY(1); break;                          \
-    case 2: SR_SKINNY(2); break;                          \
-    case 3: SR_SKINNY(3); break;                          \
-    case 4: SR_SKINNY(4); break;                          \
-    case 5: SR_SKINNY(5); break;                          \
-    case 6: SR_SKINNY(6); break;                          \
-    case 7: SR_SKINNY(7); break;                          \
-    default: SR_SKINNY(8); break;                         \
-  }
-    if (g.paired) {
-      constexpr bool PAIRED_ = true;
-      SR_SKINNY_ALL();
-    } else {
-      constexpr bool PAIRED_ = false;
-      SR_SKINNY_ALL();
-    }
-#undef SR_SKINNY_ALL
-#undef SR_SKINNY
-    SR_CHECK_LAUNCH();
-  } else if (plan.stream && dma_offsets_fit(g)) {
+  if (plan.stream && dma_offsets_fit(g)) {
     dim3 grid = tile_grid((g.M + plan.stream - 1) / plan.stream, (g.N + plan.stream_bn - 1) / plan.stream_bn, splits);
 #define SR_STREAM(BM, BN, WGM, WGN, NST, P)                                                              \
   hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, 128>), grid, dim3(256), 0, s,          \
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, \
                      part)
-    if (plan.stream_bk == 64) {
-      if (g.paired)
-        hipLaunchKernelGGL((gemm_stream_kernel<128, 64, 2, 2, 4, true, 64>), grid, dim3(256), 0, s,
-                           (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e,
-                           part);
-      else
-        hipLaunchKernelGGL((gemm_stream_kernel<128, 128, 2, 2, 4, false, 64>), grid, dim3(256), 0, s,
-                           (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e,
-                           part);
-    } else if (plan.stream == 32) {
+    if (plan.stream == 32) {
       if (g.paired) SR_STREAM(32, 64, 1, 4, 3, true);
       else SR_STREAM(32, 64, 1, 4, 5, false);
     } else if (plan.stream == 64) {

@@ -703,14 +703,33 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   int64_t generated = 0;
   std::vector<int32_t> h_done, h_i32(N);
   std::vector<float> h_f32(N);
+  // watched candidates (trace): their row in the current round, -1 if absent
+  const bool watching = tr && tr->n_watch > 0 && tr->watch_cand && tr->watch_logits;
+  std::vector<int> watch_row(watching ? tr->n_watch : 0, -1);
+  // with an end-of-sequence token, the done flags are read back every
+  // kDoneCheck steps so that a round whose rows have all finished ends there
+  constexpr int kDoneCheck = 16;
   while (true) {
     // ---- phase 1: generate up to the decision token
     tph.start();
     SR_REQUIRE((int64_t)b * cap <= pl.S[cur], SR_ERR_INTERNAL, "KV pool capacity exceeded");
+    if (watching) {
+      std::vector<int32_t> rows_cand(b);
+      copy_d2h(rows_cand.data(), L.st[cur].cand, sizeof(int32_t) * b, s);
+      for (int w = 0; w < tr->n_watch; ++w) {
+        watch_row[w] = -1;
+        for (int i = 0; i < b; ++i)
+          if (rows_cand[i] == tr->watch_cand[w]) watch_row[w] = i;
+      }
+    }
     for (; step < D; ++step) {
       prof.active = every > 0 && step % every == 0;
       const State& st = L.st[cur];
       if (step > 0) decode_step(c, G, st, b, step, L.pool[cur], pl.S[cur] * gd.hkv * gd.hd, cap);
+      for (int w = 0; w < (int)watch_row.size(); ++w)
+        if (watch_row[w] >= 0)
+          copy_d2h(tr->watch_logits + ((size_t)w * Lmax + step) * gd.V,
+                   L.logits + (step == 0 ? 0 : (size_t)watch_row[w] * gd.V), sizeof(float) * gd.V, s);
       SampleArgs sa;
       sa.logits = L.logits; sa.row_stride = step == 0 ? 0 : gd.V; sa.rows = b; sa.vocab = gd.V;
       sa.cand = st.cand; sa.step = step; sa.temperature = p->temperature; sa.seed = p->seed;
@@ -722,6 +741,14 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
           logprob_accumulate(L.logits, sa.row_stride, b, gd.V, st.cand, st.tok, st.len, step, L.lp_sum, s);
         });
       if (prof.active) prof.rotate();
+      if (p->eos_id >= 0 && (step + 1) % kDoneCheck == 0 && step + 1 < D) {
+        h_done.resize(b);
+        copy_d2h(h_done.data(), st.done, sizeof(int32_t) * b, s);
+        if (std::all_of(h_done.begin(), h_done.end(), [](int32_t v) { return v != 0; })) {
+          ++step;
+          break;
+        }
+      }
     }
     prof.active = every > 0;
     out->sec_decode += tph.stop();
@@ -735,9 +762,10 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
                        st.cand);
     SR_CHECK_LAUNCH();
     if (D == Lmax || unfinished == 0) {
-      // every candidate of this round is complete: score all, all join I
+      // every candidate of this round is complete (no row is longer than
+      // `step`): score all, all join I
       tph.start();
-      score_rows(st, b, D, cur, cap, t0);
+      score_rows(st, b, step, cur, cap, t0);
       out->sec_reward += tph.stop();
       CutArgs ca;
       std::memset(&ca, 0, sizeof(ca));
@@ -1078,6 +1106,13 @@ sr_status sr_generate(const sr_model* gen, const sr_model* rm, const int32_t* pr
     check_pair(gen, rm);
     check_params(p, gen);
     check_prompt(prompt, prompt_len, gen->cfg.vocab);
+    if (trace && trace->n_watch != 0) {
+      SR_REQUIRE(trace->n_watch > 0 && trace->watch_cand && trace->watch_logits, SR_ERR_INVALID_ARG,
+                 "trace: n_watch must be >= 0 with watch_cand and watch_logits set");
+      for (int w = 0; w < trace->n_watch; ++w)
+        SR_REQUIRE(trace->watch_cand[w] >= 0 && trace->watch_cand[w] < p->n, SR_ERR_INVALID_ARG,
+                   "trace: watch_cand entries must lie in [0, n)");
+    }
     generate(gen, rm, prompt, prompt_len, p, workspace, ws_bytes, (hipStream_t)stream, out_tokens, out,
              trace);
   });

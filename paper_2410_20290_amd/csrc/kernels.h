@@ -30,13 +30,11 @@ struct GemmArgs {
 struct GemmPlan {
   int splits;
   bool big;     // 256 x 256 tile kernel
-  bool skinny;  // weight-streaming kernel for M <= 128
   bool dma;     // 256 x 256 tile fed by LDS DMA
   int dma_bring;  // its weight ring depth: 2 (shared with the activations) or 3
   bool dma3;    // 256 x 128 tile, three LDS-DMA stages (a few hundred rows)
   int stream;     // > 0: LDS-DMA streaming kernel for few rows, tile height
   int stream_bn;  // its tile width (output columns)
-  int stream_bk;  // its K step
 };
 GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired);
 size_t gemm_partial_elems(int dtype, int M, int N, int K, bool paired);

@@ -23,27 +23,43 @@ def say(*a):
     print(*a, flush=True)
 
 
-@functools.lru_cache(maxsize=4)
+@functools.lru_cache(maxsize=2)
+def host_weights(model, gen_seed, rm_seed):
+    """Generator and reward-model weights of one shape (shared by every
+    configuration of that shape and seeds)."""
+    import synth
+    return synth.model_weights(model, gen_seed, False), synth.model_weights(model, rm_seed, True)
+
+
 def host_models(name):
     import synth
     c = synth.CONFIGS[name]
-    return (c, synth.model_weights(c.model, c.gen_seed, False), synth.model_weights(c.model, c.rm_seed, True),
-            synth.prompt(c))
+    gw, rw = host_weights(c.model, c.gen_seed, c.rm_seed)
+    return c, gw, rw, synth.prompt(c)
 
 
 _dev = {}
 
 
 def device_models(name):
-    """(config, gen, rm, prompt) with weights uploaded once per process."""
+    """(config, gen, rm, prompt) with each shape's weights uploaded once per
+    process (at most two shapes resident)."""
     torch, sr = need_gpu()
-    if name not in _dev:
-        if len(_dev) >= 2:          # keep at most two configurations resident
+    c, gw, rw, pr = host_models(name)
+    key = (c.model, c.gen_seed, c.rm_seed)
+    if key not in _dev:
+        if len(_dev) >= 2:
             _dev.pop(next(iter(_dev)))
             torch.cuda.empty_cache()
-        c, gw, rw, pr = host_models(name)
-        _dev[name] = (c, sr.DeviceModel.upload(c.model, gw, False), sr.DeviceModel.upload(c.model, rw, True), pr)
-    return _dev[name]
+        _dev[key] = (sr.DeviceModel.upload(c.model, gw, False), sr.DeviceModel.upload(c.model, rw, True))
+    return (c,) + _dev[key] + (pr,)
+
+
+def release_models():
+    """Drop every resident model (before a test that needs the memory)."""
+    torch, _ = need_gpu()
+    _dev.clear()
+    torch.cuda.empty_cache()
 
 
 def oracle_models(name):
@@ -55,3 +71,40 @@ def oracle_models(name):
 def tol(cfg):
     """Max-abs tolerance factor relative to max|x| of the oracle tensor."""
     return 1e-4 if cfg.model.dtype == "f32" else 2e-2
+
+
+def trace_rounds(out):
+    """(L, b, K, candidates, scores, accept flags) of every cut of a traced run."""
+    t = out["trace"]
+    rounds = []
+    for r in range(t["rounds"]):
+        b = int(t["round_b"][r])
+        cand = t["round_cand"][r, :b].tolist()
+        rounds.append((int(t["round_L"][r]), b, int(t["round_keep"][r]), cand,
+                       t["round_scores"][r, :b].copy(), t["round_accept"][r, :b].copy()))
+    return rounds
+
+
+def check_trace_logic(c, out):
+    """What must hold of any run, whatever the model numerics, bit for bit:
+    the keep count of every cut, the survivors = the oracle's top K on the
+    GPU's own scores (eqs. cutoff-threshold and accepted-set), the answer =
+    the oracle's arg max over the GPU's final rewards of I (eq. output), and
+    the token accounting."""
+    from oracle import specrej
+    t = out["trace"]
+    rounds = trace_rounds(out)
+    for (L, b, K, cand, scores, acc) in rounds:
+        assert K == specrej.keep_count(b, c.alpha)
+        assert cand == sorted(cand)
+        sd = {k: float(s) for k, s in zip(cand, scores)}
+        kept = set(specrej.top_k(cand, sd, K))
+        assert [int(a) for a in acc] == [1 if k in kept else 0 for k in cand]
+    fs = t["final_scores"]
+    members = {k: float(fs[k]) for k in range(c.n) if not np.isnan(fs[k])}
+    assert out["best_index"] == specrej.arg_best(members)
+    assert out["best_score"] == np.float32(members[out["best_index"]])
+    lens = t["all_len"]
+    assert out["generated_tokens"] == int(lens.sum())
+    assert out["tokens"] == t["all_tokens"][out["best_index"], : lens[out["best_index"]]].tolist()
+    return rounds

@@ -2,7 +2,9 @@
 (sr_prefill_attention) against the oracle's float64 attention on the same
 bf16 / fp32 inputs: shared prefix plus each row's own keys, ragged tails, no
 prefix, prefix only, cached history before the new tokens, every query-group
-size and head size the kernels take."""
+size and head size the kernels take.  Each row's max-abs error is bounded
+relative to the max-abs of that row of the oracle's output: 1e-2 for bf16,
+1e-5 for fp32."""
 import numpy as np
 import pytest
 
@@ -76,7 +78,7 @@ def test_decode_attention(dtype, hd, hq, hkv, rows, P, lt, cap):
         k = np.concatenate([kp.transpose(1, 0, 2), kt[r, :, :lt].transpose(1, 0, 2)], axis=0).astype(np.float64)
         v = np.concatenate([vp.transpose(1, 0, 2), vt[r, :, :lt].transpose(1, 0, 2)], axis=0).astype(np.float64)
         ref = decode_attention(q[r].astype(np.float64), k, v, hkv)
-        worst = max(worst, float(np.abs(got[r] - ref).max() / max(1.0, np.abs(ref).max())))
+        worst = max(worst, float(np.abs(got[r] - ref).max() / np.abs(ref).max()))
     tol = 1e-2 if bf16 else 1e-5
     assert worst <= tol, worst
 
@@ -126,6 +128,6 @@ def test_prefill_attention(dtype, hd, hq, hkv, rows, P, t0, lr, cap):
         qf = np.zeros((T, hq, hd))
         qf[T - lr:] = q[r]
         ref = causal_attention(qf, k, v, hkv)[T - lr:]
-        worst = max(worst, float(np.abs(got[r] - ref).max() / max(1.0, np.abs(ref).max())))
+        worst = max(worst, float(np.abs(got[r] - ref).max() / np.abs(ref).max()))
     tol = 1e-2 if bf16 else 1e-5
     assert worst <= tol, worst

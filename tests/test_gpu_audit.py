@@ -1,0 +1,153 @@
+"""Audits of whole sr_generate runs at every configuration's full size
+(section 4.2, Algorithm 1): the GPU drives and the oracle audits its trace.
+
+Bit for bit, from the run's own trace:
+  * every cut: the keep count and the survivors are the oracle's top K of the
+    GPU's scores (eqs. cutoff-threshold and accepted-set);
+  * the answer is the oracle's arg max of the GPU's final rewards over I
+    (eq. output);
+  * the rounds (L, b, K) and the token count follow the memory-budget
+    schedule in closed form;
+  * sampling: for the watched candidates (the answer, the runner-up in I and
+    the best-ranked candidate each cut rejected), the oracle's sampler applied
+    to the very logits rows the run drew from reproduces every response token
+    at every step, before and after each cut.
+Within 2e-2 of the oracle tensor's max-abs (float64 oracle, bf16 models):
+  * the run's logits at steps {0, tau - 1, tau, L_r - 1 and L_r of each cut,
+    Lmax - 1} of a few watched candidates against the oracle generator
+    teacher-forced on the same tokens;
+  * those candidates' rewards at every cut they reached and their final
+    reward, against the oracle reward model on the same prefixes.
+The float64 oracle runs every layer (weights widened one layer at a time);
+it re-runs only a few candidates of the 8B-shaped pair to stay within the
+test budget.
+"""
+import time
+
+import numpy as np
+import pytest
+
+from gpu_util import check_trace_logic, device_models, need_gpu, oracle_models, release_models, say, tol
+from oracle import sampler as osamp
+from oracle import specrej
+
+pytestmark = pytest.mark.gpu
+
+# (configuration, overrides, candidates the float64 oracle re-runs)
+AUDITS = [
+    ("small_bf16", {}, 4),
+    ("1b_bf16", {}, 2),
+    ("8b_bf16", {}, 2),
+    ("8b_bf16_n1024", {"alpha": 0.5, "tau": 64}, 1),
+    ("8b_bf16_n1024", {"alpha": 0.9, "tau": 256}, 1),
+]
+
+
+def _run(sr, c, gen, rm, prompt, watch=()):
+    p = sr.make_params(c.n, c.alpha, c.tau, c.max_new_tokens, c.temperature, c.sample_seed, c.eos_id,
+                       c.max_rounds)
+    ws = sr.Workspace(gen, rm, len(prompt), p)
+    out = sr.generate(gen, rm, prompt, p, ws, trace=True, watch=watch)
+    del ws
+    return out
+
+
+def _watch_set(c, out, rounds, n_extra=6):
+    """The answer, the runner-up of I, and the best-ranked candidate that
+    each cut rejected."""
+    t = out["trace"]
+    fs = t["final_scores"]
+    members = {k: float(fs[k]) for k in range(c.n) if not np.isnan(fs[k])}
+    order = specrej.top_k(list(members), members, len(members))
+    watch = order[:2]
+    for (L, b, K, cand, scores, acc) in rounds:
+        rej = [k for k, a in zip(cand, acc) if not a]
+        sd = {k: float(s) for k, s in zip(cand, scores)}
+        if rej:
+            watch.append(specrej.top_k(rej, sd, 1)[0])
+    seen = []
+    for k in watch:
+        if k not in seen:
+            seen.append(k)
+    return seen[:n_extra]
+
+
+def _audit_steps(c, rounds, length):
+    steps = {0, c.tau - 1, c.tau, c.max_new_tokens - 1}
+    for (L, *_rest) in rounds:
+        steps |= {L - 1, L}
+    return sorted(s for s in steps if 0 <= s < length)
+
+
+@pytest.mark.parametrize("name,over,n_oracle", AUDITS,
+                         ids=[f"{n}-" + "-".join(f"{k}{v}" for k, v in o.items()) for n, o, _ in AUDITS])
+def test_full_size_audit(name, over, n_oracle):
+    torch, sr = need_gpu()
+    t0 = time.time()
+    c, gen, rm, prompt = device_models(name)
+    c = c.with_(**over)
+    say(f"audit {c.name} {over}: N={c.n} P={c.prompt_len} tau={c.tau} alpha={c.alpha} Lmax={c.max_new_tokens}")
+    out = _run(sr, c, gen, rm, prompt)
+    rounds = check_trace_logic(c, out)
+    sched, total = specrej.schedule(c.n, c.alpha, c.tau, c.max_new_tokens)
+    assert [(L, b, K) for (L, b, K, *_rest) in rounds] == sched
+    assert out["generated_tokens"] == total
+    say(f"  run 1: {out['sec_total']:.2f}s, {len(rounds)} cuts, best {out['best_index']}")
+
+    # the same run again, recording the logits rows of the watched candidates
+    watch = _watch_set(c, out, rounds)
+    again = _run(sr, c, gen, rm, prompt, watch=watch)
+    t1, t2 = out["trace"], again["trace"]
+    assert again["best_index"] == out["best_index"] and again["best_score"] == out["best_score"]
+    assert np.array_equal(t1["all_tokens"], t2["all_tokens"]) and np.array_equal(t1["all_len"], t2["all_len"])
+    assert np.array_equal(t1["round_scores"], t2["round_scores"], equal_nan=True)
+    wl = t2["watch_logits"]
+    say(f"  run 2 (watching {watch}): {again['sec_total']:.2f}s")
+
+    # sampling, bit for bit, at every step of every watched candidate
+    for w, k in enumerate(watch):
+        n = int(t1["all_len"][k])
+        toks = t1["all_tokens"][k, :n]
+        for step in range(n):
+            assert osamp.sample(wl[w, step], c.temperature, c.sample_seed, k, step) == toks[step], (k, step)
+    say(f"  sampler reproduced {sum(int(t1['all_len'][k]) for k in watch)} tokens ({time.time() - t0:.0f}s)")
+
+    # logits and rewards of the first n_oracle watched candidates vs float64
+    P = len(prompt)
+    pl = [int(x) for x in prompt]
+    cands = watch[:n_oracle]
+    del gen, rm
+    if c.model.d_model >= 2048:
+        release_models()      # the oracle needs the host memory more than the cache
+    g, orm = oracle_models(name)
+    seqs, steps = [], []
+    for k in cands:
+        n = int(t1["all_len"][k])
+        st = _audit_steps(c, rounds, n)
+        steps.append(st)
+        seqs.append(pl + t1["all_tokens"][k, :max(st)].tolist())
+    refs = g.logits_at(seqs, [[P - 1 + s for s in st] for st in steps])
+    for w, (k, st, ref) in enumerate(zip(cands, steps, refs)):
+        for j, s in enumerate(st):
+            got = wl[watch.index(k), s]
+            assert np.abs(got - ref[j]).max() <= tol(c) * np.abs(ref[j]).max(), (k, s)
+    say(f"  logits at {sum(len(s) for s in steps)} steps match the oracle ({time.time() - t0:.0f}s)")
+    got, lens, rseqs = [], [], []
+    for k in cands:
+        ls, gs = [], []
+        for r, (L, b, K, cand, scores, acc) in enumerate(rounds):
+            if k in cand and (r == 0 or rounds[r - 1][0] != L or k not in rounds[r - 1][3]):
+                ls.append(L)
+                gs.append(float(scores[cand.index(k)]))
+        fin = float(t1["final_scores"][k])
+        n = int(t1["all_len"][k])
+        if not np.isnan(fin):
+            ls.append(n)
+            gs.append(fin)
+        lens.append([P + L for L in ls])
+        got.append(gs)
+        rseqs.append(pl + t1["all_tokens"][k, :max(ls)].tolist())
+    ref = np.concatenate(orm.scores_at(rseqs, lens))
+    got = np.concatenate([np.array(x) for x in got])
+    assert np.abs(got - ref).max() <= tol(c) * np.abs(ref).max(), (got, ref)
+    say(f"  {len(ref)} rewards match the oracle ({time.time() - t0:.0f}s)")

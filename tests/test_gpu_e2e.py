@@ -10,7 +10,7 @@ teacher-forced logits and rewards on the GPU's sequences (within 2e-2 max|x|).
 import numpy as np
 import pytest
 
-from gpu_util import device_models, host_models, need_gpu, oracle_models, say, tol
+from gpu_util import check_trace_logic, device_models, need_gpu, oracle_models, say, tol, trace_rounds
 from oracle import sampler as osamp
 from oracle import specrej
 
@@ -38,37 +38,6 @@ def gpu_run(name, reward_kind=0, reward_recompute=0, **over):
     return c, prompt, out
 
 
-def trace_rounds(out):
-    t = out["trace"]
-    rounds = []
-    for r in range(t["rounds"]):
-        b = int(t["round_b"][r])
-        cand = t["round_cand"][r, :b].tolist()
-        rounds.append((int(t["round_L"][r]), b, int(t["round_keep"][r]), cand,
-                       t["round_scores"][r, :b].copy(), t["round_accept"][r, :b].copy()))
-    return rounds
-
-
-def check_trace_logic(c, out):
-    """What must hold of any run, whatever the model numerics."""
-    t = out["trace"]
-    rounds = trace_rounds(out)
-    for (L, b, K, cand, scores, acc) in rounds:
-        assert K == specrej.keep_count(b, c.alpha)
-        assert cand == sorted(cand)
-        sd = {k: float(s) for k, s in zip(cand, scores)}
-        kept = set(specrej.top_k(cand, sd, K))
-        assert [int(a) for a in acc] == [1 if k in kept else 0 for k in cand]
-    fs = t["final_scores"]
-    members = {k: float(fs[k]) for k in range(c.n) if not np.isnan(fs[k])}
-    assert out["best_index"] == specrej.arg_best(members)
-    assert out["best_score"] == np.float32(members[out["best_index"]])
-    lens = t["all_len"]
-    assert out["generated_tokens"] == int(lens.sum())
-    assert out["tokens"] == t["all_tokens"][out["best_index"], : lens[out["best_index"]]].tolist()
-    return rounds
-
-
 @pytest.mark.parametrize("over", [{}, {"eos_id": 2}, {"max_rounds": 1}, {"alpha": 0.0},
                                   {"n": 40, "alpha": 0.1, "tau": 4, "max_new_tokens": 24}])
 def test_tiny_fp32_matches_full_oracle(over):
@@ -89,7 +58,12 @@ def test_tiny_fp32_matches_full_oracle(over):
         assert np.abs(scores - want).max() <= 1e-4 * np.abs(want).max()
         assert sorted(k for k, a in zip(cand, acc) if a) == sorted(racc)
     assert out["best_index"] == ref["best"] and out["tokens"] == ref["tokens"]
-    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * max(1.0, abs(ref["score"]))
+    final = np.array(list(ref["final"].values()))
+    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * np.abs(final).max()
+    fs = t["final_scores"]
+    assert sorted(k for k in range(c.n) if not np.isnan(fs[k])) == sorted(ref["final"])
+    got = np.array([fs[k] for k in ref["final"]])
+    assert np.abs(got - final).max() <= 1e-4 * np.abs(final).max()
     assert out["generated_tokens"] == ref["generated"]
     if c.eos_id < 0:
         assert out["generated_tokens"] == specrej.schedule(c.n, c.alpha, c.tau, c.max_new_tokens, c.max_rounds)[1]
@@ -201,10 +175,9 @@ def test_bf16_audit(name):
     # after the first score through the reward model's cached K/V)
     assert len(rounds) >= 2
     for (L0, b0, K0, cand0, sc0, acc0) in rounds:
-        for j in sorted({0, min(7, b0 - 1), b0 - 1}):
-            k = cand0[j]
-            ref = orm.score(list(prompt) + t["all_tokens"][k, :L0].tolist())
-            assert abs(sc0[j] - ref) <= tol(c) * max(abs(ref), np.abs(sc0).max()), (L0, j)
+        js = sorted({0, min(7, b0 - 1), b0 - 1})
+        refs = np.array([orm.score(list(prompt) + t["all_tokens"][cand0[j], :L0].tolist()) for j in js])
+        assert np.abs(sc0[js] - refs).max() <= tol(c) * np.abs(refs).max(), (L0, js)
     # (4) final rewards of I, recomputed by the oracle
     fs = t["final_scores"]
     mem = [k for k in range(c.n) if not np.isnan(fs[k])]
@@ -233,7 +206,8 @@ def test_tiny_fp32_logprob_reward_matches_full_oracle(over):
         assert np.abs(scores - want).max() <= 1e-4 * np.abs(want).max()
         assert sorted(k for k, a in zip(cand, acc) if a) == sorted(racc)
     assert out["best_index"] == ref["best"] and out["tokens"] == ref["tokens"]
-    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * max(1.0, abs(ref["score"]))
+    final = np.array(list(ref["final"].values()))
+    assert abs(out["best_score"] - ref["score"]) <= 1e-4 * np.abs(final).max()
 
 
 def test_profiled_run_matches_unprofiled():

@@ -1,6 +1,7 @@
 """Projection GEMM parity (sr_projection) against a float64 product of the
 same bf16/fp32 inputs, over ragged shapes, every epilogue and the split-K
-path."""
+path.  The max-abs error is bounded relative to the oracle product's
+max-abs: 1e-2 where the output is rounded to bf16, else 1e-4."""
 import numpy as np
 import pytest
 
@@ -62,6 +63,6 @@ def test_projection(dtype, mode, M, N, K):
         got = (got.view(np.uint16).astype(np.uint32) << 16).view(np.float32)
     if mode == 1:
         ref = ref + init
-    scale = max(1.0, np.abs(ref).max())
+    scale = np.abs(ref).max()
     rtol = 1e-2 if (mode in (2, 3) and dtype == "bf16") else 1e-4
     assert np.abs(got - ref).max() <= rtol * scale, np.abs(got - ref).max()

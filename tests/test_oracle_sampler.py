@@ -60,6 +60,26 @@ def test_zero_weight_never_drawn_and_threshold_below_total():
         assert sampler.sample(logits, 1.0, 3, cand, 0) not in (1, 3)
 
 
+def test_inverse_cdf_at_exact_boundaries():
+    # token = min{i : w_0 + ... + w_i > t}: a threshold equal to a cumulative
+    # weight belongs to the next token (strict inequality), and zero weights
+    # are skipped.  Hand-counted: cumulative weights 5, 8, 15.
+    w = np.array([5, 3, 7], np.uint64)
+    for t, tok in [(0, 0), (4, 0), (5, 1), (7, 1), (8, 2), (14, 2)]:
+        assert sampler.inverse_cdf(w, t) == tok, t
+    # cumulative weights 0, 4, 4, 4, 10
+    w = np.array([0, 4, 0, 0, 6], np.uint64)
+    for t, tok in [(0, 1), (3, 1), (4, 4), (9, 4)]:
+        assert sampler.inverse_cdf(w, t) == tok, t
+    # weights near 2^32 (a token of probability close to 1): exact in uint64
+    big = 2**32
+    w = np.array([big - 1, 1, big], np.uint64)
+    assert sampler.inverse_cdf(w, big - 2) == 0
+    assert sampler.inverse_cdf(w, big - 1) == 1
+    assert sampler.inverse_cdf(w, big) == 2
+    assert sampler.inverse_cdf(w, 2 * big - 1) == 2
+
+
 def test_greedy_is_first_argmax():
     logits = np.array([0.5, 2.0, -1.0, 2.0], np.float32)
     assert sampler.sample(logits, 0.0, 1, 2, 3) == 1

@@ -156,3 +156,37 @@ def test_decode_attention_is_last_causal_row_and_sdpa(hq, hkv, T):
         torch.from_numpy(q[-1:].transpose(1, 0, 2))[None], torch.from_numpy(k.transpose(1, 0, 2))[None],
         torch.from_numpy(v.transpose(1, 0, 2))[None], enable_gqa=True)[0].numpy()
     assert np.abs(got - ref[:, 0, :]).max() < 1e-12
+
+
+@pytest.mark.parametrize("cache", [True, False])
+def test_forward_many_equals_forward_of_each(cache):
+    """Sequences of different lengths through one stacked pass (weights
+    widened once per layer) give each sequence's own forward; prefix scores
+    from one pass equal the scores of the prefixes run on their own (the
+    causal mask), and logits at chosen positions equal those rows of the
+    full logits."""
+    shape = SHAPES[1]
+    gw, rw = synth.model_weights(shape, 0, False, std=0.2), synth.model_weights(shape, 1, True, std=0.2)
+    g, r = Transformer(shape, gw, False, cache_f64=cache), Transformer(shape, rw, True, cache_f64=cache)
+    seqs = [synth.tokens(n, shape.vocab, 10 + n).tolist() for n in (17, 1, 9)]
+    hs = g.forward_many(seqs)
+    for s, h in zip(seqs, hs):
+        assert h.shape == (len(s), shape.d_model)
+        assert np.abs(h - g.forward(s)).max() < 1e-12
+    pos = [[0, 5, 16], [0], [8, 3]]
+    for s, p, lg in zip(seqs, pos, g.logits_at(seqs, pos)):
+        assert np.abs(lg - g.logits(s)[p]).max() < 1e-12
+    lens = [[1, 9, 17], [1], [4, 9]]
+    for s, ls, sc in zip(seqs, lens, r.scores_at(seqs, lens)):
+        assert np.abs(sc - np.array([r.score(s[:L]) for L in ls])).max() < 1e-12
+
+
+def test_threaded_widen_is_exact():
+    rng = np.random.default_rng(11)
+    a = rng.integers(0, 1 << 16, size=(5, 1 << 20), dtype=np.uint16)
+    a[(a & 0x7F80) == 0x7F80] = 0   # no NaN patterns, so equality is well defined
+    got = widen(a)
+    ref = (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert got.shape == a.shape and np.array_equal(got, ref)
+    f = rng.normal(size=(3, 1 << 21)).astype(np.float32)
+    assert np.array_equal(widen(f), f.astype(np.float64))
