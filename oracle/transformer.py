@@ -177,12 +177,13 @@ class Transformer:
             h = h + self._ffn(h, l)
         return rmsnorm(h, self.w("final_norm"), s.rms_eps)
 
-    def forward_many(self, seqs):
+    def forward_many(self, seqs, progress=None):
         """``forward`` of several token sequences at once: the final
         normalised hidden states [T_i][d] of each.  The sequences share each
         layer's projections (their rows stacked) and attend only to
         themselves, so every layer's weights are widened once for all of
-        them (for models too large to keep widened)."""
+        them (for models too large to keep widened).  ``progress(l)`` is
+        called after layer l when given."""
         s = self.s
         seqs = [np.asarray(t, dtype=np.int64) for t in seqs]
         lens = [len(t) for t in seqs]
@@ -202,25 +203,27 @@ class Transformer:
                 o[b:e] = causal_attention(q[b:e], k[b:e], v[b:e], s.n_kv_heads)
             h = h + o.reshape(len(allt), -1) @ self.w("wo", l).T
             h = h + self._ffn(h, l)
+            if progress:
+                progress(l)
         out = rmsnorm(h, self.w("final_norm"), s.rms_eps)
         return [out[b:e] for b, e in zip(starts, ends)]
 
-    def logits_at(self, seqs, positions):
+    def logits_at(self, seqs, positions, progress=None):
         """Generator logits at chosen positions of several sequences:
         for sequence i, rows [len(positions[i])][V] with row j the
         distribution of token positions[i][j] + 1 (as ``logits``)."""
         assert not self.reward
-        hs = self.forward_many(seqs)
+        hs = self.forward_many(seqs, progress)
         head = self.w("head")
         return [h[np.asarray(p, dtype=np.int64)] @ head.T for h, p in zip(hs, positions)]
 
-    def scores_at(self, seqs, lengths):
+    def scores_at(self, seqs, lengths, progress=None):
         """Reward-model scores of prefixes: for sequence i and each length L
         in lengths[i], s(first L tokens) = w_head . out[L - 1].  Under the
         causal mask the state at position L - 1 depends only on the first L
         tokens, so one forward over the whole sequence serves every prefix."""
         assert self.reward
-        hs = self.forward_many(seqs)
+        hs = self.forward_many(seqs, progress)
         head = self.w("head")
         return [np.array([float(h[L - 1] @ head) for L in ls]) for h, ls in zip(hs, lengths)]
 

@@ -55,13 +55,6 @@ def device_models(name):
     return (c,) + _dev[key] + (pr,)
 
 
-def release_models():
-    """Drop every resident model (before a test that needs the memory)."""
-    torch, _ = need_gpu()
-    _dev.clear()
-    torch.cuda.empty_cache()
-
-
 def oracle_models(name):
     from oracle.transformer import Transformer
     c, gw, rw, pr = host_models(name)
