@@ -320,6 +320,25 @@ sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, 
 size_t sr_decode_attention_scratch(int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
                                    int32_t rows, int32_t P, int32_t lt);
 
+/* The decode attention of sr_decode_attention without a caller scratch
+ * buffer, for callers that cannot allocate device memory (code under graph
+ * capture, serving loops that forbid allocation).  Same arguments, kernels
+ * and results; the split partials go to a file-scope device array of
+ * sr_decode_attention_noalloc_limit() bytes (32 MiB) that each device holds
+ * once the library first runs this entry point on it, until the process
+ * ends.  Calls whose partials exceed it (rows * n_heads * splits *
+ * (head_dim + 2) floats, splits chosen by the kernel dispatch; up to 1024
+ * rows of 32 query heads of 128 fit) fail with SR_ERR_WORKSPACE_TOO_SMALL
+ * before any launch.  No device memory is allocated or freed.  Every call
+ * on one device shares the array: calls that overlap on a device (other
+ * streams, other threads) race and must be serialised by the caller.
+ * Asynchronous. */
+sr_status sr_decode_attention_noalloc(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                      int32_t rows, const float *q, const void *kpre, const void *vpre, int32_t P,
+                                      const void *ktail, const void *vtail, int32_t cap, int32_t lt, void *out,
+                                      void *stream);
+size_t sr_decode_attention_noalloc_limit(void);
+
 /* Causal prefill attention of `rows` rows of lr new tokens each, which follow
  * t0 tokens of the same row whose keys/values are already cached (the
  * reward model's scoring pass over the tokens generated since the previous

@@ -107,11 +107,15 @@ def lib():
                                           _vp, _vp, ctypes.c_size_t, _vp]
         L.sr_decode_attention_scratch.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32]
         L.sr_decode_attention_scratch.restype = ctypes.c_size_t
+        L.sr_decode_attention_noalloc.argtypes = [_i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
+                                                  _i32, _vp, _vp]
+        L.sr_decode_attention_noalloc_limit.argtypes = []
+        L.sr_decode_attention_noalloc_limit.restype = ctypes.c_size_t
         L.sr_prefill_attention.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _vp, _vp, _i32,
                                            _i32, _vp, _vp]
         L.sr_correlation.argtypes = [_vp, _vp, _i32, P(ctypes.c_double), P(ctypes.c_double)]
         L.sr_improvement_score.argtypes = [_vp, _i32, _f32, P(ctypes.c_double)]
-        for f in ("sr_projection", "sr_decode_attention", "sr_prefill_attention", "sr_plan_for_memory",
+        for f in ("sr_projection", "sr_decode_attention", "sr_decode_attention_noalloc", "sr_prefill_attention", "sr_plan_for_memory",
                   "sr_correlation", "sr_improvement_score", "sr_workspace_size", "sr_generate", "sr_philox_fill", "sr_sample", "sr_select", "sr_compact",
                   "sr_logits_teacher_forced", "sr_reward_scores"):
             getattr(L, f).restype = _i32
@@ -327,6 +331,23 @@ def decode_attention(q, kpre, vpre, ktail, vtail, lt: int, out, stream=None):
     _check(lib().sr_decode_attention(dtype, hd, hq, hkv, rows, _ptr(q), _ptr(kpre), _ptr(vpre), P, _ptr(ktail),
                                      _ptr(vtail), cap, lt, _ptr(out), _ptr(part), need, _stream(stream)))
     return part
+
+
+def decode_attention_noalloc(q, kpre, vpre, ktail, vtail, lt: int, out, stream=None):
+    """sr_decode_attention_noalloc: as decode_attention, with the split
+    partials in the library's static device scratch (no buffer allocated)."""
+    import torch
+    rows, hq, hd = q.shape
+    hkv, cap = ktail.shape[1], ktail.shape[2]
+    P = 0 if kpre is None else kpre.shape[1]
+    dtype = SR_BF16 if ktail.dtype in (torch.int16, torch.bfloat16) else SR_F32
+    _check(lib().sr_decode_attention_noalloc(dtype, hd, hq, hkv, rows, _ptr(q), _ptr(kpre), _ptr(vpre), P,
+                                             _ptr(ktail), _ptr(vtail), cap, lt, _ptr(out), _stream(stream)))
+
+
+def decode_attention_noalloc_limit() -> int:
+    """Bytes of the static scratch behind sr_decode_attention_noalloc."""
+    return int(lib().sr_decode_attention_noalloc_limit())
 
 
 def prefill_attention(q, kpre, vpre, kown, vown, t0: int, out, stream=None):

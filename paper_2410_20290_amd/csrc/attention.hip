@@ -12,6 +12,7 @@
 // queries of one row and one KV head; K/V tiles are staged in LDS as fp32
 // and shared by all its queries.
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -672,6 +673,56 @@ void decode_attn(const DecodeAttnArgs& a, hipStream_t s) {
   if (a.rows <= 0) return;
   if (a.dtype == SR_BF16) decode_by_hd<bf16_t>(a, s);
   else decode_by_hd<float>(a, s);
+}
+
+// Split partials (floats) the launch of decode_attn for these arguments
+// writes, following the dispatch above (without the fused QKV finalize).
+size_t decode_attn_part_floats(const DecodeAttnArgs& a) {
+  if (a.rows <= 0 || a.hkv <= 0 || a.hq % a.hkv) return 0;
+  const int g = a.hq / a.hkv;
+  const size_t per = (size_t)a.rows * a.hq * (a.hd + 2);
+  if (a.dtype == SR_BF16 && a.hd == 128 && tail_by_mfma(a.dtype, a.hd, g, a.rows)) {
+    const bool pre = prefix_by_mfma(a.dtype, a.hd, a.P, a.rows);
+    const int keys = a.P + a.lt - (pre ? a.P : 0);
+    const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
+    const int tsplits = (keys + kps - 1) / kps;
+    return (!pre && tsplits == 1) ? 0 : per * std::max(tsplits, 1);
+  }
+  if (prefix_by_mfma(a.dtype, a.hd, a.P, a.rows)) {
+    const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;
+    return per * std::max((a.lt + tkps - 1) / tkps, 1);
+  }
+  const int keys = a.P + a.lt;
+  const int kps = decode_kps(a.rows, a.hkv, keys);
+  const int splits = (keys + kps - 1) / kps;
+  return splits > 1 ? per * splits : 0;
+}
+
+// ---- decode attention without caller-provided scratch
+// For callers that cannot allocate device memory: the split partials go to
+// this file-scope array instead of a caller buffer.  Each device that runs
+// the library holds its own copy until the process ends; host code reaches
+// it only through the address hipGetSymbolAddress reports for the current
+// device (the array's name on the host is not a device address).  Every call
+// on one device shares the array, so calls that overlap on a device race.
+// Every partial slot is written before it is read, so nothing is cleared.
+static __device__ __align__(256) float scratch[kStaticScratchFloats];
+
+static std::mutex g_scratch_mu;
+static float* g_scratch_dev[kMaxDevices] = {};
+
+float* static_scratch_of_current_device() {
+  int dev = -1;
+  SR_HIP(hipGetDevice(&dev));
+  SR_REQUIRE(dev >= 0 && dev < kMaxDevices, SR_ERR_UNSUPPORTED, "device index beyond the static scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    SR_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    SR_REQUIRE(p != nullptr, SR_ERR_DEVICE, "no device address for the static scratch array");
+    g_scratch_dev[dev] = static_cast<float*>(p);
+  }
+  return g_scratch_dev[dev];
 }
 
 // --------------------------------------------------------------- prefill

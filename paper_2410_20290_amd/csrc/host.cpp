@@ -1215,32 +1215,67 @@ size_t sr_decode_attention_scratch(int32_t head_dim, int32_t n_heads, int32_t n_
   return (size_t)rows * n_heads * decode_attn_splits(rows, n_kv_heads, P + lt) * (head_dim + 2);
 }
 
+// Validated arguments of the kernel-level decode attention entry points
+// (rows == 0 leaves a.rows = 0: nothing to launch).
+static DecodeAttnArgs decode_attention_args(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                            int32_t rows, const float* q, const void* kpre, const void* vpre,
+                                            int32_t P, const void* ktail, const void* vtail, int32_t cap, int32_t lt,
+                                            void* out) {
+  SR_REQUIRE(dtype == SR_F32 || dtype == SR_BF16, SR_ERR_INVALID_ARG, "unknown dtype");
+  SR_REQUIRE(head_dim == 32 || head_dim == 64 || head_dim == 128, SR_ERR_UNSUPPORTED,
+             "head_dim must be 32, 64 or 128");
+  SR_REQUIRE(n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0, SR_ERR_INVALID_ARG, "bad head counts");
+  const int g = n_heads / n_kv_heads;
+  SR_REQUIRE(g == 1 || g == 2 || g == 4 || g == 8, SR_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8");
+  SR_REQUIRE(rows >= 0 && P >= 0 && lt >= 0 && lt <= cap && (rows == 0 || P + lt >= 1), SR_ERR_INVALID_ARG,
+             "bad rows / P / lt / cap");
+  DecodeAttnArgs a;
+  a.dtype = dtype; a.hd = head_dim; a.hq = n_heads; a.hkv = n_kv_heads; a.rows = rows; a.q = q;
+  a.kpre = kpre; a.vpre = vpre; a.P = P; a.ktail = ktail; a.vtail = vtail; a.cap = cap; a.lt = lt;
+  a.out = out; a.part = nullptr; a.part_cap = 0;
+  if (rows == 0) return a;
+  SR_REQUIRE(q && out && (P == 0 || (kpre && vpre)) && (lt == 0 || (ktail && vtail)), SR_ERR_INVALID_ARG,
+             "NULL buffer");
+  return a;
+}
+
 sr_status sr_decode_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads, int32_t rows,
                               const float* q, const void* kpre, const void* vpre, int32_t P, const void* ktail,
                               const void* vtail, int32_t cap, int32_t lt, void* out, float* scratch,
                               size_t scratch_elems, void* stream) {
   return guard([&] {
-    SR_REQUIRE(dtype == SR_F32 || dtype == SR_BF16, SR_ERR_INVALID_ARG, "unknown dtype");
-    SR_REQUIRE(head_dim == 32 || head_dim == 64 || head_dim == 128, SR_ERR_UNSUPPORTED,
-               "head_dim must be 32, 64 or 128");
-    SR_REQUIRE(n_heads >= 1 && n_kv_heads >= 1 && n_heads % n_kv_heads == 0, SR_ERR_INVALID_ARG, "bad head counts");
-    const int g = n_heads / n_kv_heads;
-    SR_REQUIRE(g == 1 || g == 2 || g == 4 || g == 8, SR_ERR_UNSUPPORTED, "query heads per KV head must be 1, 2, 4 or 8");
-    SR_REQUIRE(rows >= 0 && P >= 0 && lt >= 0 && lt <= cap && (rows == 0 || P + lt >= 1), SR_ERR_INVALID_ARG,
-               "bad rows / P / lt / cap");
+    DecodeAttnArgs a = decode_attention_args(dtype, head_dim, n_heads, n_kv_heads, rows, q, kpre, vpre, P, ktail,
+                                             vtail, cap, lt, out);
     if (rows == 0) return;
-    SR_REQUIRE(q && out && (P == 0 || (kpre && vpre)) && (lt == 0 || (ktail && vtail)), SR_ERR_INVALID_ARG,
-               "NULL buffer");
     const size_t need = sr_decode_attention_scratch(head_dim, n_heads, n_kv_heads, rows, P, lt);
     SR_REQUIRE(scratch && scratch_elems >= need, SR_ERR_WORKSPACE_TOO_SMALL,
                "attention scratch too small: need " + std::to_string(need) + " floats");
-    DecodeAttnArgs a;
-    a.dtype = dtype; a.hd = head_dim; a.hq = n_heads; a.hkv = n_kv_heads; a.rows = rows; a.q = q;
-    a.kpre = kpre; a.vpre = vpre; a.P = P; a.ktail = ktail; a.vtail = vtail; a.cap = cap; a.lt = lt;
-    a.out = out; a.part = scratch; a.part_cap = scratch_elems;
+    a.part = scratch;
+    a.part_cap = scratch_elems;
     decode_attn(a, (hipStream_t)stream);
   });
 }
+
+sr_status sr_decode_attention_noalloc(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads,
+                                      int32_t rows, const float* q, const void* kpre, const void* vpre, int32_t P,
+                                      const void* ktail, const void* vtail, int32_t cap, int32_t lt, void* out,
+                                      void* stream) {
+  return guard([&] {
+    DecodeAttnArgs a = decode_attention_args(dtype, head_dim, n_heads, n_kv_heads, rows, q, kpre, vpre, P, ktail,
+                                             vtail, cap, lt, out);
+    if (rows == 0) return;
+    const size_t need = decode_attn_part_floats(a);
+    SR_REQUIRE(need <= kStaticScratchFloats, SR_ERR_WORKSPACE_TOO_SMALL,
+               "decode attention needs " + std::to_string(need * sizeof(float)) +
+                   " bytes of partials, above the static scratch of " +
+                   std::to_string(kStaticScratchFloats * sizeof(float)) + " bytes");
+    a.part = static_scratch_of_current_device();
+    a.part_cap = kStaticScratchFloats;
+    decode_attn(a, (hipStream_t)stream);
+  });
+}
+
+size_t sr_decode_attention_noalloc_limit(void) { return kStaticScratchFloats * sizeof(float); }
 
 sr_status sr_prefill_attention(int32_t dtype, int32_t head_dim, int32_t n_heads, int32_t n_kv_heads, int32_t rows,
                                int32_t lr, const float* q, const void* kpre, const void* vpre, int32_t P,

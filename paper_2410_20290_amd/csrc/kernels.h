@@ -104,6 +104,14 @@ struct DecodeAttnArgs {
 int decode_attn_splits(int rows, int hkv, int keys);
 bool decode_attn_fuses_qkv(const DecodeAttnArgs& a);
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s);
+// Partial floats decode_attn writes for these arguments (0 when it needs none).
+size_t decode_attn_part_floats(const DecodeAttnArgs& a);
+// The file-scope scratch array of the no-allocation decode attention: its
+// size in floats, and its address on the current device (looked up once per
+// device).
+constexpr size_t kStaticScratchFloats = (size_t)8 << 20;  // 32 MiB
+constexpr int kMaxDevices = 64;
+float* static_scratch_of_current_device();
 
 // Prefill: rows of lr new tokens that follow t0 tokens already cached for
 // their row; new token (r, t) sits at response position t0 + t and attends
