@@ -26,11 +26,39 @@ w2 [nl][d][ff]; bf16 weights as uint16 bit patterns, widened exactly.
 
 The per-candidate decode state keeps a private KV cache for every row,
 prompt included: nothing is shared between candidates here.
+
+bf16 operands (``bf16_operands=True``): the same model as a bf16 model
+computes it -- the operands of every matrix product are rounded to bf16
+(round to nearest even): the normalised activations entering a projection,
+the attention output entering Wo, the SwiGLU product entering W2, the
+final normalised state entering the head, and in attention q, k (the score
+product) and the softmax probabilities and v (the value product); products
+accumulate, and everything else is computed, in float64.  The paper fixes no
+precision; this mode exists to measure how far a bf16 model drifts from the
+exact one on given inputs (the scale a bf16 implementation is compared at),
+never as the reference itself.
 """
 import os
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
+
+
+def to_bf16(x) -> np.ndarray:
+    """Round to the nearest bf16 value, ties to even (via float32: float64
+    values are first rounded to float32, as a float32 pipeline holds them),
+    returned as float64.  NaN stays NaN, infinities stay infinite, values
+    beyond the largest bf16 round to infinity."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32)
+    out = np.where(np.isnan(f), np.float32(np.nan), out)
+    return out.astype(np.float64)
+
+
+def _same(x):
+    return x
 
 
 def _widen_block(a) -> np.ndarray:
@@ -88,19 +116,21 @@ def softmax(x, axis=-1):
     return e / np.sum(e, axis=axis, keepdims=True)
 
 
-def causal_attention(q, k, v, n_kv_heads):
+def causal_attention(q, k, v, n_kv_heads, operand=_same):
     """Causal attention of one sequence: q [T][hq][hd], k, v [T][hkv][hd].
 
     Query head j reads KV head floor(j * hkv / hq); query i sees keys 0..i.
+    ``operand`` is applied to the operands of the two matrix products.
     """
     T, hq, hd = q.shape
     mask = np.triu(np.ones((T, T), dtype=bool), k=1)
+    q, k, v = operand(q), operand(k), operand(v)
     o = np.empty_like(q)
     for j in range(hq):
         kh = (j * n_kv_heads) // hq
         sc = (q[:, j, :] @ k[:, kh, :].T) / np.sqrt(hd)
         sc[mask] = -np.inf
-        o[:, j, :] = softmax(sc) @ v[:, kh, :]
+        o[:, j, :] = operand(softmax(sc)) @ v[:, kh, :]
     return o
 
 
@@ -121,10 +151,12 @@ def decode_attention(q, k, v, n_kv_heads):
 class Transformer:
     """A decoder given by a shape (see ``synth.ModelShape``) and weights."""
 
-    def __init__(self, shape, weights: dict, reward: bool, cache_f64: bool = None):
+    def __init__(self, shape, weights: dict, reward: bool, cache_f64: bool = None, bf16_operands: bool = False):
         self.s = shape
         self.reward = reward
         self.raw = weights
+        self.bf16_operands = bf16_operands
+        self.op = to_bf16 if bf16_operands else _same
         nparams = sum(int(np.prod(np.shape(v))) for v in weights.values())
         self.cache_f64 = (nparams * 8 < (4 << 30)) if cache_f64 is None else cache_f64
         self._c = {}
@@ -150,11 +182,11 @@ class Transformer:
 
     def _ffn(self, h, l):
         s = self.s
-        f = rmsnorm(h, self.w("ffn_norm", l), s.rms_eps)
+        f = self.op(rmsnorm(h, self.w("ffn_norm", l), s.rms_eps))
         w13 = self.w("w13", l)
         gate = f @ w13[0].T
         up = f @ w13[1].T
-        return (silu(gate) * up) @ self.w("w2", l).T
+        return self.op(silu(gate) * up) @ self.w("w2", l).T
 
     def kv_head_of(self, j):
         return (j * self.s.n_kv_heads) // self.s.n_heads
@@ -169,11 +201,11 @@ class Transformer:
         cos, sin = rope_cos_sin(np.arange(T), s.head_dim, s.rope_theta)
         cos, sin = cos[:, None, :], sin[:, None, :]
         for l in range(s.n_layers):
-            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            a = self.op(rmsnorm(h, self.w("attn_norm", l), s.rms_eps))
             q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
             q, k = rope(q, cos, sin), rope(k, cos, sin)
-            o = causal_attention(q, k, v, s.n_kv_heads)
-            h = h + o.reshape(T, -1) @ self.w("wo", l).T
+            o = causal_attention(q, k, v, s.n_kv_heads, self.op)
+            h = h + self.op(o.reshape(T, -1)) @ self.w("wo", l).T
             h = h + self._ffn(h, l)
         return rmsnorm(h, self.w("final_norm"), s.rms_eps)
 
@@ -195,13 +227,13 @@ class Transformer:
         cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta)
         cos, sin = cos[:, None, :], sin[:, None, :]
         for l in range(s.n_layers):
-            a = rmsnorm(h, self.w("attn_norm", l), s.rms_eps)
+            a = self.op(rmsnorm(h, self.w("attn_norm", l), s.rms_eps))
             q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
             q, k = rope(q, cos, sin), rope(k, cos, sin)
             o = np.empty_like(q)
             for b, e in zip(starts, ends):
-                o[b:e] = causal_attention(q[b:e], k[b:e], v[b:e], s.n_kv_heads)
-            h = h + o.reshape(len(allt), -1) @ self.w("wo", l).T
+                o[b:e] = causal_attention(q[b:e], k[b:e], v[b:e], s.n_kv_heads, self.op)
+            h = h + self.op(o.reshape(len(allt), -1)) @ self.w("wo", l).T
             h = h + self._ffn(h, l)
             if progress:
                 progress(l)
@@ -215,7 +247,7 @@ class Transformer:
         assert not self.reward
         hs = self.forward_many(seqs, progress)
         head = self.w("head")
-        return [h[np.asarray(p, dtype=np.int64)] @ head.T for h, p in zip(hs, positions)]
+        return [self.op(h[np.asarray(p, dtype=np.int64)]) @ head.T for h, p in zip(hs, positions)]
 
     def scores_at(self, seqs, lengths, progress=None):
         """Reward-model scores of prefixes: for sequence i and each length L
@@ -225,18 +257,18 @@ class Transformer:
         assert self.reward
         hs = self.forward_many(seqs, progress)
         head = self.w("head")
-        return [np.array([float(h[L - 1] @ head) for L in ls]) for h, ls in zip(hs, lengths)]
+        return [np.array([float(self.op(h[L - 1]) @ head) for L in ls]) for h, ls in zip(hs, lengths)]
 
     def logits(self, tokens):
         """Generator logits [T][V]: row t is the distribution of token t+1."""
         assert not self.reward
-        return self.forward(tokens) @ self.w("head").T
+        return self.op(self.forward(tokens)) @ self.w("head").T
 
     def score(self, tokens) -> float:
         """Reward model s(x, y): scalar head on the last token's state."""
         assert self.reward
         out = self.forward(tokens)
-        return float(out[-1] @ self.w("head"))
+        return float(self.op(out[-1]) @ self.w("head"))
 
     # -- batched incremental decoding with private caches ---------------
     def start(self, prompt, rows: int, capacity: int):
@@ -247,6 +279,7 @@ class Transformer:
         ``capacity`` bounds prompt plus response length.
         Returns (state, logits of the last prompt position [V]).
         """
+        assert not self.bf16_operands, "bf16 operands: whole-sequence forwards only"
         s = self.s
         prompt = np.asarray(prompt, dtype=np.int64)
         P = len(prompt)
@@ -280,6 +313,7 @@ class Transformer:
 
     def step(self, state, tokens):
         """Append one token per row at position state['pos']; return logits [rows][V]."""
+        assert not self.bf16_operands, "bf16 operands: whole-sequence forwards only"
         s = self.s
         tokens = np.asarray(tokens, dtype=np.int64)
         rows = len(tokens)

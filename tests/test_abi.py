@@ -30,7 +30,7 @@ def declared_symbols():
 
 def test_header_symbols_exported(L):
     names = declared_symbols()
-    assert len(names) == 18, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(L, n), n
 

@@ -190,3 +190,47 @@ def test_threaded_widen_is_exact():
     assert got.shape == a.shape and np.array_equal(got, ref)
     f = rng.normal(size=(3, 1 << 21)).astype(np.float32)
     assert np.array_equal(widen(f), f.astype(np.float64))
+
+
+def test_to_bf16_rounds_like_torch():
+    """The bf16 rounding of the oracle's bf16-operand mode equals torch's
+    float32 -> bfloat16 conversion (round to nearest even), specials included."""
+    from oracle.transformer import to_bf16
+    rng = np.random.default_rng(5)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-30, 30, 20000),
+                        np.array([0.0, -0.0, np.inf, -np.inf, 3.3895313892515355e38, -3.4e38, 1e-40, -1e-45])])
+    x = x.astype(np.float32)
+    # exact ties: low 16 bits 0x8000 with even and odd kept parts
+    ties = (np.array([0x3F808000, 0x3F818000, 0xBF808000, 0x00018000], dtype=np.uint32)).view(np.float32)
+    x = np.concatenate([x, ties])
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = to_bf16(x)
+    assert np.array_equal(got, ref) and np.array_equal(np.signbit(got), np.signbit(ref))
+    assert np.isnan(to_bf16(np.array([np.nan]))[0])
+    # float64 input is held as float32 first
+    y = rng.standard_normal(1000)
+    assert np.array_equal(to_bf16(y), torch.from_numpy(y).float().to(torch.bfloat16).double().numpy())
+
+
+def test_bf16_operands_drift_is_bf16_sized_and_like_hf_autocast():
+    """The bf16-operand mode is a bf16 model: on a 4-layer model its logits
+    leave the exact model's by a bf16-sized amount (not zero, well below 5 %),
+    of the same size as HF Llama's under torch's bf16 autocast (an independent
+    bf16 evaluation, within a factor of 3)."""
+    shape = synth.ModelShape(4, 256, 8, 2, 32, 512, 500, "bf16", 10000.0)
+    w = synth.model_weights(shape, 0, False, std=0.05)
+    toks = synth.tokens(96, shape.vocab, 3)
+    ex = Transformer(shape, w, False).logits(toks)
+    bm = Transformer(shape, w, False, bf16_operands=True).logits(toks)
+    m = hf_model(shape, w, False).float()
+    with torch.no_grad(), torch.autocast("cpu", dtype=torch.bfloat16):
+        hf = m(torch.from_numpy(np.asarray(toks, dtype=np.int64))[None]).logits[0].float().numpy()
+    sc = np.abs(ex).max()
+    ours, theirs = np.abs(bm - ex).max() / sc, np.abs(hf - ex).max() / sc
+    assert 2.0 ** -12 < ours < 5e-2, ours
+    assert 1 / 3 < ours / theirs < 3, (ours, theirs)
+    # scores too, through the same mode
+    rw = synth.model_weights(shape, 1, True, std=0.05)
+    se = Transformer(shape, rw, True).scores_at([toks], [[10, 50, 96]])[0]
+    sb = Transformer(shape, rw, True, bf16_operands=True).scores_at([toks], [[10, 50, 96]])[0]
+    assert 0 < np.abs(sb - se).max() < 5e-2 * np.abs(se).max()
