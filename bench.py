@@ -65,31 +65,102 @@ def load_traffic(kernel_class):
     return {"bytes_per_launch": d["traffic_bytes_per_launch"], "source": os.path.relpath(path, ROOT)}
 
 
-def cpu_baseline(cfg, gw, rows, steps, prompt_len):
-    """The oracle's batched decode on the same generator, bounded sample."""
+def _cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count()
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
+    except Exception:
+        threads = nproc
+    return model, nproc, threads
+
+
+def cpu_baseline(cfg, gw, rw, kind, rows=4, steps=2, full_below=5e7):
+    """The oracle on the host cores.  Small models: the oracle's whole
+    Speculative Rejection run, timed end to end.  Large ones: a bounded
+    sample, extrapolated to one prompt with the schedule's closed-form step
+    counts -- the prompt forward of the generator (untimed weight widening
+    beforehand), which gives the cost of a forward pass per token, and
+    `steps` decode steps at `rows` candidates, which gives the cost of a
+    decode step when the weights, not the rows, bound it; a decode step of
+    b rows is charged max(that, b x the per-token forward cost), a reward
+    round of b rows at length L b x (P + L) tokens of forward (the oracle
+    scores every partial sequence from its first token, with the same-shape
+    reward model, or with the generator for the mean log-probability)."""
     import numpy as np
 
+    import synth
+    from oracle import specrej
     from oracle.sampler import sample
     from oracle.transformer import Transformer
 
-    g = Transformer(cfg.model, gw, False, cache_f64=True)
-    prompt = list(range(1, prompt_len + 1))
-    state, l0 = g.start(prompt, rows, prompt_len + steps + 1)   # widens weights (not timed)
-    toks = [sample(np.float32(l0), 1.0, 42, k, 0) for k in range(rows)]
+    model, nproc, threads = _cpu_info()
+    m = cfg.model
+    prompt = [int(x) for x in synth.prompt(cfg)]
+    P = len(prompt)
+    nparams = sum(int(np.prod(np.shape(v))) for v in gw.values())
+    base = {"unit": "tokens/s", "cores": threads, "nproc": nproc, "cpu_model": model, "kind": "oracle"}
+    if nparams < full_below:
+        g = Transformer(m, gw, False)
+        r = None if kind == "logprob" else Transformer(m, rw, True)
+        lp = (lambda pr, toks: specrej.mean_logprob(g, pr, toks)) if kind == "logprob" else None
+        t0 = time.perf_counter()
+        out = specrej.speculative_rejection(g, r, prompt, cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens,
+                                            cfg.temperature, cfg.sample_seed, cfg.eos_id, cfg.max_rounds,
+                                            score_fn=lp)
+        dt = time.perf_counter() - t0
+        return dict(base, value=round(out["generated"] / dt, 4), s_per_prompt=round(dt, 3),
+                    sample=f"the oracle's whole run (float64 numpy), {out['generated']} tokens in {dt:.1f} s")
+    g = Transformer(m, gw, False, cache_f64=True)
+    for name in ("embed", "final_norm", "head"):
+        g.w(name)
+    for name in ("attn_norm", "wqkv", "wo", "ffn_norm", "w13", "w2"):
+        for l in range(m.n_layers):
+            g.w(name, l)
+    t0 = time.perf_counter()
+    state, l0 = g.start(prompt, rows, P + steps + 1)
+    t_prompt = time.perf_counter() - t0
+    toks = [sample(np.float32(l0), cfg.temperature, cfg.sample_seed, k, 0) for k in range(rows)]
     t0 = time.perf_counter()
     for s in range(1, steps + 1):
         lg = g.step(state, toks)
-        toks = [sample(np.float32(lg[k]), 1.0, 42, k, s) for k in range(rows)]
-    dt = time.perf_counter() - t0
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max(i.get("num_threads", 1) for i in threadpool_info()) or 1
-    except Exception:
-        cores = os.cpu_count()
-    return {"value": round(rows * steps / dt, 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"oracle float64 decode of {rows} candidates x {steps} steps on the same generator "
-                      f"(prompt prefix of {prompt_len} tokens, weights widened beforehand, untimed); "
-                      f"{dt:.1f} s"}
+        toks = [sample(np.float32(lg[k]), cfg.temperature, cfg.sample_seed, k, s) for k in range(rows)]
+    t_step = (time.perf_counter() - t0) / steps
+    c_tok = t_prompt / P
+
+    def extrapolate(alpha):
+        rounds, total = specrej.schedule(cfg.n, alpha, cfg.tau, cfg.max_new_tokens, cfg.max_rounds)
+        sec, b, L = t_prompt, cfg.n, 0
+        for (Lr, br, K) in rounds + [(cfg.max_new_tokens, None, None)]:
+            sec += (Lr - L) * max(t_step, b * c_tok)
+            L = Lr
+            if br is None:
+                break
+            sec += br * (P + Lr) * c_tok
+            b = K
+        sec += b * (P + cfg.max_new_tokens) * c_tok
+        return sec, total
+
+    sr_s, sr_tokens = extrapolate(cfg.alpha)
+    bon_s, _ = extrapolate(0.0)
+    return dict(base, value=round(sr_tokens / sr_s, 4), s_per_prompt=round(sr_s, 1),
+                bon_s_per_prompt=round(bon_s, 1), extrapolated=True,
+                sample=f"extrapolated: oracle (float64 numpy) prompt forward of {P} tokens {t_prompt:.1f} s and "
+                       f"{steps} decode steps at {rows} candidates {t_step:.2f} s each, weights widened beforehand "
+                       f"(untimed); a step of b rows costs max({t_step:.2f} s, b x {c_tok:.3f} s), a reward round "
+                       f"b x (P + L) tokens x {c_tok:.3f} s, over the schedule's rounds")
 
 
 def main():
@@ -103,8 +174,11 @@ def main():
     ap.add_argument("--profile-every", type=int, default=64)
     ap.add_argument("--no-bon", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=8)
-    ap.add_argument("--cpu-steps", type=int, default=48)
+    ap.add_argument("--bon-runs", type=int, default=3, help="timed Best-of-N runs after one warm-up (median)")
+    ap.add_argument("--cpu-rows", type=int, default=4)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--max-new-tokens", type=int, default=None,
+                    help="shorter responses (for counter runs of the same kernels; not a bench line)")
     ap.add_argument("--reward", choices=["model", "logprob"], default="model",
                     help="partial reward: the reward model, or the generator's mean log-probability "
                          "(section 5.3, no reward model)")
@@ -127,7 +201,10 @@ def main():
     import paper_2410_20290_amd as sr
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    cfg = synth.CONFIGS[args.config]
+    configs = dict(synth.CONFIGS, **{c.name: c for c in synth.SWEEP_8B_N1024})
+    cfg = configs[args.config]
+    if args.max_new_tokens is not None:
+        cfg = cfg.with_(max_new_tokens=args.max_new_tokens)
     if args.alpha is not None:
         cfg = cfg.with_(alpha=args.alpha)
     if args.tau is not None:
@@ -141,7 +218,8 @@ def main():
     kind = sr.SR_REWARD_LOGPROB if args.reward == "logprob" else sr.SR_REWARD_MODEL
     gen = sr.DeviceModel.upload(m, gw, False)
     rm = sr.DeviceModel.upload(m, rw, True) if kind == sr.SR_REWARD_MODEL else None
-    del rw
+    if sum(int(np.prod(np.shape(v))) for v in gw.values()) >= 5e7:
+        rw = None   # the CPU leg runs the whole oracle only for small models
     torch.cuda.synchronize()
     log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
 
@@ -183,6 +261,7 @@ def main():
     elapsed = time.perf_counter() - t0
     s_per_prompt = elapsed / args.steps
     value = gen_tokens / elapsed
+    s_median = float(np.median([o["sec_total"] for o in results]))
     del ws
     torch.cuda.empty_cache()
 
@@ -191,15 +270,22 @@ def main():
         pb = sr.make_params(cfg.n, 0.0, cfg.tau, cfg.max_new_tokens, cfg.temperature, cfg.sample_seed,
                             cfg.eos_id, 0, 0, kind, rrc)
         wsb = sr.Workspace(gen, rm, len(prompt), pb)
-        torch.cuda.synchronize()
-        tb = time.perf_counter()
-        ob = sr.generate(gen, rm, prompt, pb, wsb, trace=True)
-        torch.cuda.synchronize()
-        tb = time.perf_counter() - tb
-        bon = {"s_per_prompt": round(tb, 4), "tokens_per_s": round(ob["generated_tokens"] / tb, 1),
+        ob = sr.generate(gen, rm, prompt, pb, wsb, trace=True)   # warm-up (and the trace)
+        log(f"[bench] best-of-N (alpha=0) warm-up: {ob['sec_total']:.3f}s")
+        times = []
+        for i in range(max(1, args.bon_runs)):
+            torch.cuda.synchronize()
+            tb = time.perf_counter()
+            o = sr.generate(gen, rm, prompt, pb, wsb)
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - tb)
+            assert o["best_index"] == ob["best_index"]
+            log(f"[bench] best-of-N (alpha=0) run {i}: {times[-1]:.3f}s")
+        tb = float(np.median(times))
+        bon = {"s_per_prompt": round(tb, 4), "runs_s": [round(x, 4) for x in times], "warmup": 1,
+               "tokens_per_s": round(ob["generated_tokens"] / tb, 1),
                "generated_tokens": ob["generated_tokens"], "best_index": ob["best_index"],
                "sr_best_index": results[-1]["best_index"]}
-        log(f"[bench] best-of-N (alpha=0): {tb:.3f}s")
         if warm is not None and warm["trace"]["rounds"] > 0:
             # section 5 and Appendix B diagnostics: the first cut's partial
             # rewards against Best-of-N's final rewards of the same candidates
@@ -240,20 +326,28 @@ def main():
         if tr:
             roof["traffic"] = tr["bytes_per_launch"]
             roof["traffic_source"] = tr["source"]
+    # the stated per-class goals at the 8B shape, with what this run reached
+    targets = {}
+    for name, goal in (("decode_attn", 0.70), ("gen_gemm_mfma", 0.50), ("rm_gemm", 0.50)):
+        if name in kernels:
+            targets[name] = {"frac": kernels[name]["frac"], "target": goal, "unit": kernels[name]["unit"],
+                             "met": kernels[name]["frac"] >= goal}
 
     cpu = None
     if not args.no_cpu:
         del gen, rm
         torch.cuda.empty_cache()
-        log("[bench] timing the CPU oracle sample")
-        cpu = cpu_baseline(cfg, gw, args.cpu_rows, args.cpu_steps, 16)
+        log("[bench] timing the CPU oracle")
+        cpu = cpu_baseline(cfg, gw, rw, args.reward, args.cpu_rows, args.cpu_steps)
+        log(f"[bench] CPU oracle: {cpu['sample']}")
 
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(s_per_prompt * 1e3, 2), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": m.dtype, "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: 8B-shaped bf16 generator + "
-                               + ("reward model" if kind == sr.SR_REWARD_MODEL else
+        "config": {"workload": f"{cfg.name}: {m.dtype} generator ({m.n_layers} layers, d {m.d_model}, "
+                               f"{m.n_heads}/{m.n_kv_heads} heads x {m.head_dim}, ffn {m.ffn_dim}, vocab {m.vocab}) + "
+                               + ("reward model of the same shape" if kind == sr.SR_REWARD_MODEL else
                                   "mean log-probability reward (no reward model)")
                                + f", prompt {cfg.prompt_len}, "
                                f"N={cfg.n}, tau={cfg.tau}, alpha={cfg.alpha}, {cfg.max_new_tokens} new tokens",
@@ -264,12 +358,20 @@ def main():
                    "N": cfg.n, "alpha": cfg.alpha, "tau": cfg.tau, "max_new_tokens": cfg.max_new_tokens,
                    "prompt_len": cfg.prompt_len},
         "s_per_prompt": round(s_per_prompt, 4),
+        "s_per_prompt_median": round(s_median, 4),
         "generated_tokens_per_prompt": results[-1]["generated_tokens"],
         "phases_s": {k: round(results[-1][k], 4) for k in ("sec_prefill", "sec_decode", "sec_reward", "sec_cut")},
         "best_of_n": bon,
         "speedup_vs_alpha0": round(bon["s_per_prompt"] / s_per_prompt, 3) if bon else None,
         "roofline": roof,
+        "targets": targets,
         "kernels": kernels,
+        "paper_context": "The paper reports Speculative Rejection as 16-32x more efficient than Best-of-N "
+                         "(abstract; section 5.1): Best-of-N needs 16 to 32 GPUs to reach the reward Speculative "
+                         "Rejection reaches on one, on a DGX node of H100 80 GB GPUs (Llama-3-8B generator, "
+                         "Mistral-7B reward model, AlpacaFarm-Eval prompts).  That ratio compares against Best-of-N "
+                         "at larger N on several GPUs and is not comparable to speedup_vs_alpha0 (alpha=0 at the "
+                         "same N on one GPU).",
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -28,60 +28,66 @@ The per-candidate decode state keeps a private KV cache for every row,
 prompt included: nothing is shared between candidates here.
 
 bf16 operands (``bf16_operands=True``): the same model as a bf16 model
-computes it -- the operands of every matrix product are rounded to bf16
-(round to nearest even): the normalised activations entering a projection,
-the attention output entering Wo, the SwiGLU product entering W2, the
-final normalised state entering the head, and in attention q, k (the score
-product) and the softmax probabilities and v (the value product); products
-accumulate, and everything else is computed, in float64.  The paper fixes no
+computes it in mixed precision -- the operands of every matrix product are
+rounded to bf16 (round to nearest even): the normalised activations entering
+a projection, the attention output entering Wo, the SwiGLU product entering
+W2, the final normalised state entering the head, and in attention q, k (the
+score product) and the softmax probabilities and v (the value product);
+products accumulate, and everything else is computed, in float32.  The paper fixes no
 precision; this mode exists to measure how far a bf16 model drifts from the
 exact one on given inputs (the scale a bf16 implementation is compared at),
 never as the reference itself.
 """
+import math
 import os
 from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
 
-def to_bf16(x) -> np.ndarray:
+def to_bf16(x, dtype=np.float64) -> np.ndarray:
     """Round to the nearest bf16 value, ties to even (via float32: float64
     values are first rounded to float32, as a float32 pipeline holds them),
-    returned as float64.  NaN stays NaN, infinities stay infinite, values
+    returned as `dtype`.  NaN stays NaN, infinities stay infinite, values
     beyond the largest bf16 round to infinity."""
     f = np.asarray(x, dtype=np.float32)
     u = f.view(np.uint32).astype(np.uint64)
     r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
     out = r.astype(np.uint32).view(np.float32)
     out = np.where(np.isnan(f), np.float32(np.nan), out)
-    return out.astype(np.float64)
+    return out.astype(dtype)
+
+
+def _to_bf16_f32(x) -> np.ndarray:
+    return to_bf16(x, np.float32)
 
 
 def _same(x):
     return x
 
 
-def _widen_block(a) -> np.ndarray:
+def _widen_block(a, dtype=np.float64) -> np.ndarray:
     if a.dtype == np.uint16:
-        return (a.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-    return a.astype(np.float64)
+        return (a.astype(np.uint32) << 16).view(np.float32).astype(dtype)
+    return a.astype(dtype)
 
 
-def widen(a) -> np.ndarray:
-    """Weights as float64 (bf16 bit patterns are widened exactly).  Large
-    arrays are widened in row blocks on several threads (numpy's casts run
-    without the interpreter lock); the result is the same."""
+def widen(a, dtype=np.float64) -> np.ndarray:
+    """Weights as float64 (or `dtype`; bf16 bit patterns are widened
+    exactly).  Large arrays are widened in row blocks on several threads
+    (numpy's casts run without the interpreter lock); the result is the
+    same."""
     a = np.asarray(a)
     if a.ndim == 0 or a.size < (1 << 22):
-        return _widen_block(a)
-    out = np.empty(a.shape, dtype=np.float64)
+        return _widen_block(a, dtype)
+    out = np.empty(a.shape, dtype=dtype)
     flat_in, flat_out = a.reshape(-1), out.reshape(-1)
     n = flat_in.size
     parts = min(32, os.cpu_count() or 1)
     step = -(-n // parts)
 
     def one(i):
-        flat_out[i * step:(i + 1) * step] = _widen_block(flat_in[i * step:(i + 1) * step])
+        flat_out[i * step:(i + 1) * step] = _widen_block(flat_in[i * step:(i + 1) * step], dtype)
 
     with ThreadPoolExecutor(parts) as ex:
         list(ex.map(one, range(parts)))
@@ -128,7 +134,7 @@ def causal_attention(q, k, v, n_kv_heads, operand=_same):
     o = np.empty_like(q)
     for j in range(hq):
         kh = (j * n_kv_heads) // hq
-        sc = (q[:, j, :] @ k[:, kh, :].T) / np.sqrt(hd)
+        sc = (q[:, j, :] @ k[:, kh, :].T) / math.sqrt(hd)
         sc[mask] = -np.inf
         o[:, j, :] = operand(softmax(sc)) @ v[:, kh, :]
     return o
@@ -156,7 +162,8 @@ class Transformer:
         self.reward = reward
         self.raw = weights
         self.bf16_operands = bf16_operands
-        self.op = to_bf16 if bf16_operands else _same
+        self.op = _to_bf16_f32 if bf16_operands else _same
+        self.ft = np.float32 if bf16_operands else np.float64   # arithmetic type
         nparams = sum(int(np.prod(np.shape(v))) for v in weights.values())
         self.cache_f64 = (nparams * 8 < (4 << 30)) if cache_f64 is None else cache_f64
         self._c = {}
@@ -167,7 +174,7 @@ class Transformer:
         if key in self._c:
             return self._c[key]
         a = self.raw[name] if layer is None else self.raw[name][layer]
-        a = widen(a)
+        a = widen(a, self.ft)
         if self.cache_f64:
             self._c[key] = a
         return a
@@ -197,9 +204,9 @@ class Transformer:
         s = self.s
         tokens = np.asarray(tokens, dtype=np.int64)
         T = len(tokens)
-        h = self.w("embed")[tokens] if self.cache_f64 else widen(self.raw["embed"][tokens])
+        h = self.w("embed")[tokens] if self.cache_f64 else widen(self.raw["embed"][tokens], self.ft)
         cos, sin = rope_cos_sin(np.arange(T), s.head_dim, s.rope_theta)
-        cos, sin = cos[:, None, :], sin[:, None, :]
+        cos, sin = cos[:, None, :].astype(self.ft), sin[:, None, :].astype(self.ft)
         for l in range(s.n_layers):
             a = self.op(rmsnorm(h, self.w("attn_norm", l), s.rms_eps))
             q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)
@@ -222,10 +229,10 @@ class Transformer:
         ends = np.cumsum(lens)
         starts = ends - np.asarray(lens)
         allt = np.concatenate(seqs)
-        h = self.w("embed")[allt] if self.cache_f64 else widen(self.raw["embed"][allt])
+        h = self.w("embed")[allt] if self.cache_f64 else widen(self.raw["embed"][allt], self.ft)
         pos = np.concatenate([np.arange(T) for T in lens])
         cos, sin = rope_cos_sin(pos, s.head_dim, s.rope_theta)
-        cos, sin = cos[:, None, :], sin[:, None, :]
+        cos, sin = cos[:, None, :].astype(self.ft), sin[:, None, :].astype(self.ft)
         for l in range(s.n_layers):
             a = self.op(rmsnorm(h, self.w("attn_norm", l), s.rms_eps))
             q, k, v = self._split_qkv(a @ self.w("wqkv", l).T)

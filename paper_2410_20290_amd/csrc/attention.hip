@@ -48,6 +48,22 @@ __device__ __forceinline__ float group_sum(float d) {
   }
 }
 
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Every lane names 8 bytes
+// (four bf16); within each group of 16 lanes, element e of lane i's result
+// is element (i & 3) of the four named by lane 4 e + (i >> 2).
+__device__ __forceinline__ i16x4 lds_read_tr16(const bf16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
+// two transpose reads as one MFMA operand (the 16-bit words reinterpreted
+// as a whole vector)
+__device__ __forceinline__ bf16x8 tr16_pair(i16x4 lo, i16x4 hi) {
+  const i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, w);
+}
+
 template <typename T, int HD, int G>
 __global__ void __launch_bounds__(256)
 decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, const T* __restrict__ vpre,
@@ -480,6 +496,305 @@ decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ 
   }
 }
 
+// ------------------------------------------------ decode (waves split keys)
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  else static_assert(N < 0, "add this wait count");
+}
+
+// 16-byte chunk slot of chunk c of key k (k = key index within a 32-key V
+// block) in the LDS copy: XOR-swizzled so that the transpose reads of a
+// wave (four consecutive keys per lane group, two chunks each) spread over
+// the banks.
+template <int CPK>
+__device__ __forceinline__ int vslot(int k, int c) {
+  if constexpr (CPK == 16) return c ^ (((k & 3) << 1) | (((k >> 2) & 1) << 3));
+  else return c ^ ((k & 3) << 1);
+}
+
+// Decode attention over keys [key0, P + lt) for bf16, head_dim 64 or 128,
+// on MFMA, with the keys split between the NW waves of a work-group (and
+// between `splits` work-groups per (row, KV head)): each wave streams its
+// own contiguous run of kpw keys in 32-key blocks and waits on no other wave
+// until the final merge.  Work-group = (split, KV head, row); the G query
+// heads of the KV head are the MFMA's 16 columns (columns >= G are zero
+// queries whose results are dropped).
+//   S^T = K Q^T: the A operand (16 keys x 32 dims) is loaded from memory
+//         straight into registers, 16 bytes of one key row per lane.
+//   O^T += V^T P^T: a V block is copied memory -> LDS (global_load_lds into
+//         the wave's own double buffer) and the A operand (16 dims x 32
+//         keys) comes from two LDS transpose reads; the key order of the
+//         contraction is permuted so that the B operand is the lane's own 8
+//         probabilities (keys 4 (l/16) + i and 16 + 4 (l/16) + i).
+// The K loads and V copy of the next block are in flight while a block is
+// computed.  Online softmax in base 2 (q carries log2 e / sqrt(hd)).  The
+// waves' (max, sum, unnormalised output) are merged through LDS; the
+// work-group writes the output or, with several splits, its partial slot.
+// Fused QKV finalize as in decode_tail_mfma_kernel: the wave that holds the
+// newest key writes its K (rotated) and V row before it loads any key.
+template <int HD, int G, int NW>
+__global__ void __launch_bounds__(64 * NW)
+decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
+                   int P, bf16_t* ktail, bf16_t* vtail, int cap, int lt, int hq, int hkv, int kpw, int key0,
+                   int splits, float* __restrict__ part, bf16_t* __restrict__ out, float qscale,
+                   const float* __restrict__ qpart, int qsplits, int qkv_dim, const float2* __restrict__ rope,
+                   float* __restrict__ qout) {
+  constexpr int KS = HD / 32;           // k-steps of the score product
+  constexpr int DT = HD / 16;           // 16-dim tiles of the output
+  constexpr int CPK = HD / 8;           // 16-byte chunks per key row
+  constexpr int VB = 32 * HD;           // bf16 elements of a 32-key V block
+  constexpr int NDMA = VB * 2 / 1024;   // 1 KB copies per V block
+  constexpr int KPD = 64 / CPK;         // keys per copy
+  constexpr int INFLIGHT = 2 * KS + NDMA;  // memory operations of one block
+  static_assert(HD == 64 || HD == 128, "head_dim");
+  static_assert(G >= 1 && G <= 16, "query heads per KV head");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NW * 2 * VB];
+  const int split = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const int total = P + lt;
+  const int w0 = key0 + (split * NW + wave) * kpw;
+  const int w1 = min(total, w0 + kpw);
+  const int nb = w0 < w1 ? (w1 - w0 + 31) >> 5 : 0;
+  const bf16_t* kt = ktail + ((int64_t)row * hkv + h) * cap * HD;
+  const bf16_t* vt = vtail + ((int64_t)row * hkv + h) * cap * HD;
+  const bf16_t* kp = kpre + (int64_t)h * P * HD;
+  const bf16_t* vp = vpre + (int64_t)h * P * HD;
+  bf16_t* vbuf = lds + wave * 2 * VB;
+
+  // fused QKV finalize: the newest key's K (rotated) and V row
+  const bool writer = qpart && nb > 0 && w1 == total;
+  if (writer) {
+    const int64_t qs = (int64_t)gridDim.z * qkv_dim;
+    const float* pk = qpart + (int64_t)row * qkv_dim + (hq + h) * HD;
+    const float* pv = pk + hkv * HD;
+    const int64_t at = (((int64_t)row * hkv + h) * cap + lt - 1) * HD;
+    for (int d = lane; d < HD / 2; d += 64) {
+      float k1v = 0.f, k2v = 0.f, v1 = 0.f, v2 = 0.f;
+      for (int sp = 0; sp < qsplits; ++sp) {
+        k1v += pk[sp * qs + d];
+        k2v += pk[sp * qs + HD / 2 + d];
+        v1 += pv[sp * qs + d];
+        v2 += pv[sp * qs + HD / 2 + d];
+      }
+      const float2 c = rope[d];
+      ktail[at + d] = f32_to_bf16(k1v * c.x - k2v * c.y);
+      ktail[at + HD / 2 + d] = f32_to_bf16(k2v * c.x + k1v * c.y);
+      vtail[at + d] = f32_to_bf16(v1);
+      vtail[at + HD / 2 + d] = f32_to_bf16(v2);
+    }
+    vm_wait<0>();
+  }
+
+  // Q^T fragments (B operand): lane holds Q[query fr][32 s + 8 fg .. + 8],
+  // scaled, bf16.  Fused: the rotation pairs (d, d + hd/2) are the lane's
+  // k-steps s and s + KS/2.
+  bf16x8 qf[KS];
+  {
+    const bool qvalid = fr < G;
+    const int qh = h * G + (qvalid ? fr : 0);
+    float x[KS][8];
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[st][e] = 0.f;
+    if (qpart) {
+      const int64_t qs = (int64_t)gridDim.z * qkv_dim;
+      const float* pq = qpart + (int64_t)row * qkv_dim + qh * HD + 8 * fg;
+      if (qvalid)
+        for (int sp = 0; sp < qsplits; ++sp) {
+#pragma unroll
+          for (int st = 0; st < KS; ++st) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(pq + sp * qs + 32 * st);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(pq + sp * qs + 32 * st + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              x[st][e] += a[e];
+              x[st][4 + e] += b[e];
+            }
+          }
+        }
+      float* qo = qout && split == 0 && wave == 0 && qvalid ? qout + ((int64_t)row * hq + qh) * HD : nullptr;
+#pragma unroll
+      for (int st = 0; st < KS / 2; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int d = 32 * st + 8 * fg + e;
+          const float x1 = x[st][e], x2 = x[st + KS / 2][e];
+          const float2 c = rope[d];
+          x[st][e] = x1 * c.x - x2 * c.y;
+          x[st + KS / 2][e] = x2 * c.x + x1 * c.y;
+          if (qo) {
+            qo[d] = x[st][e];
+            qo[HD / 2 + d] = x[st + KS / 2][e];
+          }
+        }
+    } else if (qvalid) {
+      const float* qr = q + ((int64_t)row * hq + qh) * HD;
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[st][e] = qr[32 * st + 8 * fg + e];
+    }
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[st][e] = (__bf16)(qvalid ? x[st][e] * qscale : 0.f);
+  }
+
+  auto load_k = [&](int b, uint4 (&kr)[2][KS]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int j = min(w0 + 32 * b + 16 * t + fr, w1 - 1);
+      const bf16_t* src = j < P ? kp + (int64_t)j * HD : kt + (int64_t)(j - P) * HD;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) kr[t][st] = *reinterpret_cast<const uint4*>(src + 32 * st + 8 * fg);
+    }
+  };
+  auto copy_v = [&](int b, int buf) {
+    bf16_t* dst = vbuf + buf * VB;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const int kk = i * KPD + lane / CPK;
+      const int c = vslot<CPK>(kk, lane % CPK);
+      const int j = min(w0 + 32 * b + kk, w1 - 1);
+      const bf16_t* src = (j < P ? vp + (int64_t)j * HD : vt + (int64_t)(j - P) * HD) + 8 * c;
+      dma16(reinterpret_cast<const char*>(src), dst + i * 512);
+    }
+  };
+
+  f32x4 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  // transpose-read addresses: lane names 4 dims (dt 16 + 4 (fr & 3) ..) of
+  // key 4 fg + (fr >> 2), and of the key 16 on
+  const int kr0 = 4 * fg + (fr >> 2), kr1 = kr0 + 16;
+  auto compute = [&](int b, const uint4 (&kr)[2][KS], int buf) {
+    f32x4 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2)
+        st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[t][s2]), qf[s2], st[t], 0, 0,
+                                                        0);
+    }
+    const int jb = w0 + 32 * b + 4 * fg;
+    float sv[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sv[i] = jb + i < w1 ? st[0][i] : -INFINITY;
+      sv[4 + i] = jb + 16 + i < w1 ? st[1][i] : -INFINITY;
+    }
+    float mt = sv[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sv[i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m, mt);
+    const bool none = mn == -INFINITY;
+    const float corr = none ? 1.f : exp2f(m - mn);
+    bf16x8 pf;
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float pv = none ? 0.f : exp2f(sv[i] - mn);
+      ps += pv;
+      pf[i] = (__bf16)pv;
+    }
+    l = l * corr + ps;
+    m = mn;
+    const bf16_t* vs = vbuf + buf * VB;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int c = 2 * dt + ((fr & 3) >> 1), e4 = 4 * (fr & 1);
+      const i16x4 lo = lds_read_tr16(vs + kr0 * HD + 8 * vslot<CPK>(kr0, c) + e4);
+      const i16x4 hi = lds_read_tr16(vs + kr1 * HD + 8 * vslot<CPK>(kr1, c) + e4);
+      o[dt] *= corr;
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tr16_pair(lo, hi), pf, o[dt], 0, 0, 0);
+    }
+  };
+
+  if (nb > 0) {
+    uint4 ka[2][KS], kb[2][KS];
+    load_k(0, ka);
+    copy_v(0, 0);
+    for (int b = 0; b < nb; b += 2) {
+      if (b + 1 < nb) {
+        load_k(b + 1, kb);
+        copy_v(b + 1, 1);
+        vm_wait<INFLIGHT>();
+      } else {
+        vm_wait<0>();
+      }
+      compute(b, ka, 0);
+      if (b + 1 < nb) {
+        asm volatile("" ::: "memory");
+        if (b + 2 < nb) {
+          load_k(b + 2, ka);
+          copy_v(b + 2, 0);
+          vm_wait<INFLIGHT>();
+        } else {
+          vm_wait<0>();
+        }
+        compute(b + 1, kb, 1);
+        asm volatile("" ::: "memory");
+      }
+    }
+  }
+
+  // merge the waves: per query (max, sum, unnormalised output)
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  __syncthreads();
+  float* sm = reinterpret_cast<float*>(lds);  // [NW][G][HD + 2]
+  if (fr < G) {
+    float* w = sm + (wave * G + fr) * (HD + 2);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[dt * 16 + 4 * fg + i] = o[dt][i];
+    if (fg == 0) {
+      w[HD] = m;
+      w[HD + 1] = l;
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < G * HD; idx += 64 * NW) {
+    const int g = idx / HD, d = idx % HD;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm[(w * G + g) * (HD + 2) + HD]);
+    float L = 0.f, A = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float* ws = sm + (w * G + g) * (HD + 2);
+        const float c = exp2_or_zero(ws[HD] - M);
+        L += ws[HD + 1] * c;
+        A += ws[d] * c;
+      }
+    }
+    const int qh = h * G + g;
+    if (splits == 1 && out) {
+      out[((int64_t)row * hq + qh) * HD + d] = f32_to_bf16(A / L);
+    } else {
+      float* pp = part + (((int64_t)row * hq + qh) * splits + split) * (HD + 2);
+      pp[d] = A;
+      if (d == 0) {
+        pp[HD] = M;
+        pp[HD + 1] = L;
+      }
+    }
+  }
+}
+
 template <typename T, int HD>
 __global__ void decode_merge_kernel(const float* __restrict__ part, int splits, T* __restrict__ out) {
   const int rq = blockIdx.x;  // row * hq + qh
@@ -506,6 +821,9 @@ static int decode_kps(int rows, int hkv, int keys) {
   return (keys + splits - 1) / splits;
 }
 
+// Waves decode_wave_kernel aims at over the whole grid.
+constexpr int kWaveTarget = 2048;
+
 // Keys per split for the MFMA streaming kernel: as many splits as keep the
 // grid within one round of resident work-groups (two per CU), at least 64
 // keys per split (a partly filled second round measured slower).
@@ -517,7 +835,7 @@ static int tail_mfma_kps(int rows, int hkv, int keys) {
   return (keys + splits - 1) / splits;
 }
 
-template <int G, bool PREFIX_ONLY>
+template <int HD, int G, bool PREFIX_ONLY>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
                                          const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq,
@@ -536,7 +854,11 @@ int decode_attn_splits(int rows, int hkv, int keys) {
   int kps = decode_kps(rows, hkv, keys);
   const int old_form = (keys + kps - 1) / kps + (keys + 63) / 64;
   const int dma_form = keys > 0 ? (keys + tail_mfma_kps(rows, hkv, keys) - 1) / tail_mfma_kps(rows, hkv, keys) : 0;
-  return std::max(old_form, dma_form + (keys + 63) / 64);
+  // the key-split kernel: splits <= the waves it wants per (row, KV head),
+  // which grow with the key count
+  const int64_t pairs = std::max<int64_t>(1, (int64_t)rows * hkv);
+  const int wave_form_max = (int)std::max<int64_t>(1, std::min<int64_t>(kWaveTarget / pairs, (keys + 31) / 32));
+  return std::max({old_form, dma_form + (keys + 63) / 64, wave_form_max});
 }
 
 // Whether the MFMA streaming kernel takes the keys (bf16, head_dim 128, up to
@@ -565,6 +887,48 @@ static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsp
   SR_CHECK_LAUNCH();
 }
 
+// Work split of decode_wave_kernel over `keys` keys of rows x hkv (row, KV
+// head) pairs: about kWaveTarget waves in all (one round of resident waves:
+// LDS holds ten per CU at head_dim 128), each with at least two 32-key
+// blocks; NW waves per work-group (1, 2 or 4) and `splits` work-groups per
+// pair, each wave kpw keys (a multiple of 32).
+struct WavePlan {
+  int nw, splits, kpw;
+};
+static WavePlan wave_plan(int rows, int hkv, int keys) {
+  const int64_t pairs = std::max<int64_t>(1, (int64_t)rows * hkv);
+  const int blocks = std::max(1, (keys + 31) / 32);
+  int want = (int)std::max<int64_t>(1, kWaveTarget / pairs);
+  want = std::max(1, std::min(want, blocks / 2));
+  WavePlan w;
+  w.nw = want >= 4 ? 4 : (want >= 2 ? 2 : 1);
+  const int per = (want + w.nw - 1) / w.nw * w.nw;    // waves per pair
+  w.kpw = 32 * ((blocks + per - 1) / per);
+  w.splits = std::max(1, (keys + w.nw * w.kpw - 1) / (w.nw * w.kpw));
+  return w;
+}
+
+// Whether decode_wave_kernel takes these keys (bf16, head_dim 64 or 128,
+// 1, 2, 4 or 8 query heads per KV head).
+static bool wave_form(int dtype, int hd, int g) {
+  return dtype == SR_BF16 && (hd == 64 || hd == 128) && (g == 1 || g == 2 || g == 4 || g == 8);
+}
+
+template <int HD, int G>
+static void launch_wave(const DecodeAttnArgs& a, int key0, const WavePlan& w, bool direct, float qscale,
+                        hipStream_t s) {
+#define SR_WAVE(NW)                                                                                              \
+  hipLaunchKernelGGL((decode_wave_kernel<HD, G, NW>), dim3(w.splits, a.hkv, a.rows), dim3(64 * NW), 0, s, a.q,  \
+                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail,       \
+                     a.cap, a.lt, a.hq, a.hkv, w.kpw, key0, w.splits, a.part, direct ? (bf16_t*)a.out : nullptr, \
+                     qscale, a.qpart, a.qsplits, a.qkv_dim, a.rope, a.qout)
+  if (w.nw == 4) SR_WAVE(4);
+  else if (w.nw == 2) SR_WAVE(2);
+  else SR_WAVE(1);
+#undef SR_WAVE
+  SR_CHECK_LAUNCH();
+}
+
 template <typename T, int HD, int G>
 static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
@@ -572,11 +936,42 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   // runs last: the tails leave partial slots and it folds them into its own
   // result, so no merge pass is needed.
   auto prefix_pass = [&](int tsplits) {
-    hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
+    hipLaunchKernelGGL((prefill_attn_mfma_kernel<128, G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
                        a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows, 0, 0, a.hq,
                        a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
     SR_CHECK_LAUNCH();
   };
+  if constexpr (HD == 64 || HD == 128) {
+    if (wave_form(a.dtype, HD, G)) {
+      // the key-split kernel over the keys past the prefix pass's, then the
+      // prefix pass or (several splits without it) the merge
+      const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
+      SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), SR_ERR_INTERNAL,
+                 "fused QKV finalize needs a new key");
+      const int key0 = pre ? a.P : 0;
+      const int keys = a.P + a.lt - key0;
+      if (keys > 0) {
+        const WavePlan w = wave_plan(a.rows, a.hkv, keys);
+        const bool direct = !pre && w.splits == 1;
+        if (!direct)
+          SR_REQUIRE((size_t)a.rows * a.hq * w.splits * (HD + 2) <= a.part_cap, 5,
+                     "attention partial buffer too small");
+        DecodeAttnArgs b = a;
+        if (!pre) b.qout = nullptr;  // only the prefix pass reads q back
+        launch_wave<HD, G>(b, key0, w, direct, qscale, s);
+        if (pre) {
+          prefix_pass(w.splits);
+        } else if (!direct) {
+          hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, w.splits,
+                             (T*)a.out);
+          SR_CHECK_LAUNCH();
+        }
+      } else {
+        prefix_pass(0);
+      }
+      return;
+    }
+  }
   if (tail_by_mfma(a.dtype, HD, G, a.rows)) {
     // the streaming kernel over the keys past the prefix pass's, then the
     // prefix pass or (several splits without it) the merge
@@ -666,7 +1061,8 @@ static void decode_by_hd(const DecodeAttnArgs& a, hipStream_t s) {
 bool decode_attn_fuses_qkv(const DecodeAttnArgs& a) {
   if (a.hkv <= 0 || a.hq % a.hkv) return false;
   const int g = a.hq / a.hkv;
-  return (g == 1 || g == 2 || g == 4 || g == 8) && a.lt >= 1 && tail_by_mfma(a.dtype, a.hd, g, a.rows);
+  return (g == 1 || g == 2 || g == 4 || g == 8) && a.lt >= 1 &&
+         (wave_form(a.dtype, a.hd, g) || tail_by_mfma(a.dtype, a.hd, g, a.rows));
 }
 
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s) {
@@ -681,6 +1077,13 @@ size_t decode_attn_part_floats(const DecodeAttnArgs& a) {
   if (a.rows <= 0 || a.hkv <= 0 || a.hq % a.hkv) return 0;
   const int g = a.hq / a.hkv;
   const size_t per = (size_t)a.rows * a.hq * (a.hd + 2);
+  if (wave_form(a.dtype, a.hd, g)) {
+    const bool pre = prefix_by_mfma(a.dtype, a.hd, a.P, a.rows);
+    const int keys = a.P + a.lt - (pre ? a.P : 0);
+    if (keys <= 0) return 0;
+    const WavePlan w = wave_plan(a.rows, a.hkv, keys);
+    return (!pre && w.splits == 1) ? 0 : per * w.splits;
+  }
   if (a.dtype == SR_BF16 && a.hd == 128 && tail_by_mfma(a.dtype, a.hd, g, a.rows)) {
     const bool pre = prefix_by_mfma(a.dtype, a.hd, a.P, a.rows);
     const int keys = a.P + a.lt - (pre ? a.P : 0);
@@ -817,7 +1220,8 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 
 
 // --------------------------------------------------------- prefill (MFMA)
-// bf16 flash attention with v_mfma_f32_16x16x32_bf16.  Work-group = one row,
+// bf16 flash attention with v_mfma_f32_16x16x32_bf16, head_dim 64 or 128.
+// Work-group = one row,
 // one KV head, 16 queries; wave w computes query head (kvh * G + w) for those
 // queries, so the G waves share every K/V tile staged in LDS (32 keys).
 //   S^T = K Q^T   (keys x queries): lane l holds keys 4(l/16)+i (+16 for the
@@ -829,25 +1233,6 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 //                 operand comes from the V tile, staged row by row like K, by
 //                 two LDS transpose reads.
 constexpr int PF_KT = 32;            // keys per tile
-constexpr int PF_KROW = 128 + 8;     // K tile row (bf16), padded
-constexpr int PF_VROW = 128 + 16;    // V tile row (bf16), padded: the 8-byte transpose reads of a
-                                     // half wave (eight rows) fall on distinct banks
-
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef short i16x8 __attribute__((ext_vector_type(8)));
-
-// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Every lane names 8 bytes
-// (four bf16); within each group of 16 lanes, element e of lane i's result
-// is element (i & 3) of the four named by lane 4 e + (i >> 2).
-__device__ __forceinline__ i16x4 lds_read_tr16(const bf16_t* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
-}
-// two transpose reads as one MFMA operand (the 16-bit words reinterpreted
-// as a whole vector)
-__device__ __forceinline__ bf16x8 tr16_pair(i16x4 lo, i16x4 hi) {
-  const i16x8 w = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return __builtin_bit_cast(bf16x8, w);
-}
 
 // PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
 // The 16 "queries" of a work-group are 16 decode rows (lr = rows, one
@@ -858,13 +1243,18 @@ __device__ __forceinline__ bf16x8 tr16_pair(i16x4 lo, i16x4 hi) {
 // The prefix form fetches the next 32-key tile into registers while the
 // current one is computed (the prefill form, with many work-groups per CU,
 // fetches each tile just before staging it).
-template <int G, bool PREFIX_ONLY>
+template <int HD, int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
                          const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq, int hkv,
                          bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
-  constexpr int HD = 128, NT = 64 * G;
+  constexpr int NT = 64 * G;
+  constexpr int KS = HD / 32, DT = HD / 16, CPK = HD / 8;
+  constexpr int PF_KROW = HD + 8;    // K tile row (bf16), padded
+  constexpr int PF_VROW = HD + 16;   // V tile row (bf16), padded: the 8-byte transpose reads of a
+                                     // half wave (eight rows) fall on distinct banks
+  static_assert(HD == 64 || HD == 128, "head_dim");
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[PF_KT * PF_VROW];
   const int qb = blockIdx.x, h = blockIdx.y, row = PREFIX_ONLY ? 0 : blockIdx.z;
@@ -874,20 +1264,20 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   const int t = qb * 16 + fr;              // this lane's query (as B column / C column)
   const bool qvalid = t < lr;
   // Q^T fragments: lane holds Q[t][32 s + 8 fg .. +8] for k-step s (scaled, bf16)
-  bf16x8 qf[4];
+  bf16x8 qf[KS];
   {
     const float* qr = q + (((int64_t)row * lr + (qvalid ? t : 0)) * hq + qh) * HD;
 #pragma unroll
-    for (int st = 0; st < 4; ++st)
+    for (int st = 0; st < KS; ++st)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float v = qvalid ? qr[32 * st + 8 * fg + e] * qscale : 0.f;
         qf[st][e] = (__bf16)v;
       }
   }
-  f32x4 o[8];
+  f32x4 o[DT];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
   const int tlast = min(lr, (qb + 1) * 16) - 1;
   const int nkeys = PREFIX_ONLY ? P : P + t0 + tlast + 1;
@@ -895,16 +1285,16 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
   const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * cap * HD;
   const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * cap * HD;
-  // a tile is 32 keys x 16 chunks of 8 dims; thread chunks c = tid + NT i
-  constexpr int CPT = (PF_KT * 16 + NT - 1) / NT;
+  // a tile is 32 keys x CPK chunks of 8 dims; thread chunks c = tid + NT i
+  constexpr int CPT = (PF_KT * CPK + NT - 1) / NT;
   uint4 kreg[CPT], vreg[CPT];
   auto fetch = [&](int kb) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = threadIdx.x + NT * i;
-      const int key = kb + (c >> 4), cc = c & 15;
+      const int key = kb + c / CPK, cc = c % CPK;
       kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
-      if (c < PF_KT * 16 && key < nkeys) {
+      if (c < PF_KT * CPK && key < nkeys) {
         const bf16_t* kr = key < P ? kp + (int64_t)key * HD : ko + (int64_t)(key - P) * HD;
         const bf16_t* vr = key < P ? vp + (int64_t)key * HD : vo + (int64_t)(key - P) * HD;
         kreg[i] = *reinterpret_cast<const uint4*>(kr + cc * 8);
@@ -919,8 +1309,8 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = threadIdx.x + NT * i;
-      if (c >= PF_KT * 16) break;
-      const int j = c >> 4, cc = c & 15;
+      if (c >= PF_KT * CPK) break;
+      const int j = c / CPK, cc = c % CPK;
       *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
       *reinterpret_cast<uint4*>(&Vs[j * PF_VROW + cc * 8]) = vreg[i];
     }
@@ -933,7 +1323,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     for (int kt = 0; kt < 2; ++kt) {
       st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
+      for (int s = 0; s < KS; ++s) {
         const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(kt * 16 + fr) * PF_KROW + 32 * s + 8 * fg]);
         st[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[kt], 0, 0, 0);
       }
@@ -973,7 +1363,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     // 16 + 4 fg .. + 3): the A operand rows
     const bf16_t* vb = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
+    for (int dt = 0; dt < DT; ++dt) {
       o[dt] *= corr;
       const i16x4 lo = lds_read_tr16(vb + dt * 16);
       const i16x4 hi = lds_read_tr16(vb + 16 * PF_VROW + dt * 16);
@@ -991,27 +1381,27 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       const float c0 = exp2_or_zero(m - mx);
       float L = l * c0;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) o[dt] *= c0;
+      for (int dt = 0; dt < DT; ++dt) o[dt] *= c0;
       for (int sp = 0; sp < part_splits; ++sp) {
         const float* ps = pr + sp * (HD + 2);
         const float cs = exp2_or_zero(ps[HD] - mx);
         L += ps[HD + 1] * cs;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) o[dt][i] += ps[dt * 16 + 4 * fg + i] * cs;
       }
       const float inv = 1.0f / L;
       bf16_t* orow = out + ((int64_t)t * hq + qh) * HD;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
     } else {
       const float inv = 1.0f / l;
       bf16_t* orow = out + (((int64_t)row * lr + t) * hq + qh) * HD;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt)
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) orow[dt * 16 + 4 * fg + i] = f32_to_bf16(o[dt][i] * inv);
     }
@@ -1050,11 +1440,11 @@ static void prefill_by_hd(const PrefillAttnArgs& a, hipStream_t s) {
   }
 }
 
-template <int G>
+template <int HD, int G>
 static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
-  const float qscale = kLog2e / sqrtf(128.f);
+  const float qscale = kLog2e / sqrtf((float)HD);
   dim3 grid((a.lr + 15) / 16, a.hkv, a.rows);
-  hipLaunchKernelGGL((prefill_attn_mfma_kernel<G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
+  hipLaunchKernelGGL((prefill_attn_mfma_kernel<HD, G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
                      (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.cap, a.t0,
                      a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();
@@ -1064,10 +1454,19 @@ void prefill_attn(const PrefillAttnArgs& a, hipStream_t s) {
   if (a.rows <= 0 || a.lr <= 0) return;
   if (a.dtype == SR_BF16 && a.hd == 128) {
     switch (a.hq / a.hkv) {
-      case 1: launch_prefill_mfma<1>(a, s); return;
-      case 2: launch_prefill_mfma<2>(a, s); return;
-      case 4: launch_prefill_mfma<4>(a, s); return;
-      case 8: launch_prefill_mfma<8>(a, s); return;
+      case 1: launch_prefill_mfma<128, 1>(a, s); return;
+      case 2: launch_prefill_mfma<128, 2>(a, s); return;
+      case 4: launch_prefill_mfma<128, 4>(a, s); return;
+      case 8: launch_prefill_mfma<128, 8>(a, s); return;
+      default: break;
+    }
+  }
+  if (a.dtype == SR_BF16 && a.hd == 64) {
+    switch (a.hq / a.hkv) {
+      case 1: launch_prefill_mfma<64, 1>(a, s); return;
+      case 2: launch_prefill_mfma<64, 2>(a, s); return;
+      case 4: launch_prefill_mfma<64, 4>(a, s); return;
+      case 8: launch_prefill_mfma<64, 8>(a, s); return;
       default: break;
     }
   }

@@ -55,10 +55,11 @@ def device_models(name):
     return (c,) + _dev[key] + (pr,)
 
 
-def oracle_models(name):
+def oracle_models(name, bf16_operands=False):
     from oracle.transformer import Transformer
     c, gw, rw, pr = host_models(name)
-    return Transformer(c.model, gw, False), Transformer(c.model, rw, True)
+    return (Transformer(c.model, gw, False, bf16_operands=bf16_operands),
+            Transformer(c.model, rw, True, bf16_operands=bf16_operands))
 
 
 def tol(cfg):
