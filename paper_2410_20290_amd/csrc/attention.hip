@@ -567,8 +567,38 @@ decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
   bf16_t* vbuf = lds + wave * 2 * VB;
 
-  // fused QKV finalize: the newest key's K (rotated) and V row
+  auto load_k = [&](int b, uint4 (&kr)[2][KS]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int j = min(w0 + 32 * b + 16 * t + fr, w1 - 1);
+      const bf16_t* src = j < P ? kp + (int64_t)j * HD : kt + (int64_t)(j - P) * HD;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) kr[t][st] = *reinterpret_cast<const uint4*>(src + 32 * st + 8 * fg);
+    }
+  };
+  auto copy_v = [&](int b, int buf) {
+    bf16_t* dst = vbuf + buf * VB;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const int kk = i * KPD + lane / CPK;
+      const int c = vslot<CPK>(kk, lane % CPK);
+      const int j = min(w0 + 32 * b + kk, w1 - 1);
+      const bf16_t* src = (j < P ? vp + (int64_t)j * HD : vt + (int64_t)(j - P) * HD) + 8 * c;
+      dma16(reinterpret_cast<const char*>(src), dst + i * 512);
+    }
+  };
+
+  // The first block's loads go out before anything else unless it holds
+  // the newest key, which this wave writes first (fused QKV finalize).
   const bool writer = qpart && nb > 0 && w1 == total;
+  const bool early = nb > 0 && !(writer && nb == 1);
+  uint4 ka[2][KS], kb[2][KS];
+  if (early) {
+    load_k(0, ka);
+    copy_v(0, 0);
+  }
+
+  // fused QKV finalize: the newest key's K (rotated) and V row
   if (writer) {
     const int64_t qs = (int64_t)gridDim.z * qkv_dim;
     const float* pk = qpart + (int64_t)row * qkv_dim + (hq + h) * HD;
@@ -647,27 +677,6 @@ decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
       for (int e = 0; e < 8; ++e) qf[st][e] = (__bf16)(qvalid ? x[st][e] * qscale : 0.f);
   }
 
-  auto load_k = [&](int b, uint4 (&kr)[2][KS]) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int j = min(w0 + 32 * b + 16 * t + fr, w1 - 1);
-      const bf16_t* src = j < P ? kp + (int64_t)j * HD : kt + (int64_t)(j - P) * HD;
-#pragma unroll
-      for (int st = 0; st < KS; ++st) kr[t][st] = *reinterpret_cast<const uint4*>(src + 32 * st + 8 * fg);
-    }
-  };
-  auto copy_v = [&](int b, int buf) {
-    bf16_t* dst = vbuf + buf * VB;
-#pragma unroll
-    for (int i = 0; i < NDMA; ++i) {
-      const int kk = i * KPD + lane / CPK;
-      const int c = vslot<CPK>(kk, lane % CPK);
-      const int j = min(w0 + 32 * b + kk, w1 - 1);
-      const bf16_t* src = (j < P ? vp + (int64_t)j * HD : vt + (int64_t)(j - P) * HD) + 8 * c;
-      dma16(reinterpret_cast<const char*>(src), dst + i * 512);
-    }
-  };
-
   f32x4 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -722,9 +731,10 @@ decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
   };
 
   if (nb > 0) {
-    uint4 ka[2][KS], kb[2][KS];
-    load_k(0, ka);
-    copy_v(0, 0);
+    if (!early) {
+      load_k(0, ka);
+      copy_v(0, 0);
+    }
     for (int b = 0; b < nb; b += 2) {
       if (b + 1 < nb) {
         load_k(b + 1, kb);
@@ -890,8 +900,10 @@ static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsp
 // Work split of decode_wave_kernel over `keys` keys of rows x hkv (row, KV
 // head) pairs: about kWaveTarget waves in all (one round of resident waves:
 // LDS holds ten per CU at head_dim 128), each with at least two 32-key
-// blocks; NW waves per work-group (1, 2 or 4) and `splits` work-groups per
-// pair, each wave kpw keys (a multiple of 32).
+// blocks; NW waves per work-group (1, 2, 4 or 8) and `splits` work-groups
+// per pair, each wave kpw keys (a multiple of 32).  Where eight waves per
+// pair already give a thousand waves, one work-group of eight takes the pair
+// (no split partials, no merge launch).
 struct WavePlan {
   int nw, splits, kpw;
 };
@@ -900,8 +912,9 @@ static WavePlan wave_plan(int rows, int hkv, int keys) {
   const int blocks = std::max(1, (keys + 31) / 32);
   int want = (int)std::max<int64_t>(1, kWaveTarget / pairs);
   want = std::max(1, std::min(want, blocks / 2));
+  if (want > 8 && pairs * 8 >= 1024) want = 8;
   WavePlan w;
-  w.nw = want >= 4 ? 4 : (want >= 2 ? 2 : 1);
+  w.nw = want >= 8 ? 8 : (want >= 4 ? 4 : (want >= 2 ? 2 : 1));
   const int per = (want + w.nw - 1) / w.nw * w.nw;    // waves per pair
   w.kpw = 32 * ((blocks + per - 1) / per);
   w.splits = std::max(1, (keys + w.nw * w.kpw - 1) / (w.nw * w.kpw));
@@ -922,7 +935,8 @@ static void launch_wave(const DecodeAttnArgs& a, int key0, const WavePlan& w, bo
                      (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail,       \
                      a.cap, a.lt, a.hq, a.hkv, w.kpw, key0, w.splits, a.part, direct ? (bf16_t*)a.out : nullptr, \
                      qscale, a.qpart, a.qsplits, a.qkv_dim, a.rope, a.qout)
-  if (w.nw == 4) SR_WAVE(4);
+  if (w.nw == 8) SR_WAVE(8);
+  else if (w.nw == 4) SR_WAVE(4);
   else if (w.nw == 2) SR_WAVE(2);
   else SR_WAVE(1);
 #undef SR_WAVE
