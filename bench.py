@@ -163,6 +163,84 @@ def cpu_baseline(cfg, gw, rw, kind, rows=4, steps=2, full_below=5e7):
                        f"b x (P + L) tokens x {c_tok:.3f} s, over the schedule's rounds")
 
 
+def counter_workload(cfg, gen, rm, prompt, case="all"):
+    """The hot path's kernels at the configuration's shapes in runs short
+    enough for rocprofv3 --pmc (which does not complete a whole call of the
+    8B-shaped pair on this software stack): one calibration kernel of known
+    bytes; the generator's decode step (the library's own decode path, via
+    sr_logits_teacher_forced) at every row count of the schedule; decode
+    attention (sr_decode_attention) at each decode phase's row count and mean
+    tail length; the reward model's four projections (sr_projection) at the
+    row count of a scoring chunk.  `case` picks one group ("decode",
+    "attention", "rm") or all; prints what ran, one line per case."""
+    import numpy as np
+    import torch
+
+    import paper_2410_20290_amd as sr
+    from oracle.specrej import schedule
+
+    m = cfg.model
+    dev = "cuda"
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+    print(json.dumps({"case": "calibration", "read_bytes": 1 << 30, "write_bytes": 1 << 30}), flush=True)
+    rounds, _ = schedule(cfg.n, cfg.alpha, cfg.tau, cfg.max_new_tokens, cfg.max_rounds)
+    phases, L = [], 0
+    b = cfg.n
+    for (Lr, br, K) in rounds + [(cfg.max_new_tokens, None, None)]:
+        phases.append((b, L, Lr))
+        L = Lr
+        if K is not None:
+            b = K
+    P = len(prompt)
+    steps = 8
+    for (rows, L0, L1) in (phases if case in ("all", "decode") else []):
+        p = sr.make_params(rows, 0.0, steps, steps)
+        ws = sr.Workspace(gen, rm, P, p)
+        toks = torch.from_numpy(np.random.default_rng(0).integers(0, m.vocab, size=(rows, steps)).astype(np.int32))
+        out = sr.logits_teacher_forced(gen, rm, prompt, p, toks.to(dev), ws)
+        torch.cuda.synchronize()
+        del out, ws
+        torch.cuda.empty_cache()
+        print(json.dumps({"case": "decode_step", "rows": rows, "steps": steps}), flush=True)
+    bf = torch.bfloat16
+    for (rows, L0, L1) in (phases if case in ("all", "attention") else []):
+        lt = (L0 + L1) // 2
+        cap = (lt + 63) // 64 * 64
+        q = torch.randn(rows, m.n_heads, m.head_dim, device=dev)
+        kp = torch.randn(m.n_kv_heads, P, m.head_dim, device=dev).to(bf).view(torch.int16)
+        vp = torch.randn(m.n_kv_heads, P, m.head_dim, device=dev).to(bf).view(torch.int16)
+        kt = torch.randn(rows, m.n_kv_heads, cap, m.head_dim, device=dev).to(bf).view(torch.int16)
+        vt = torch.randn(rows, m.n_kv_heads, cap, m.head_dim, device=dev).to(bf).view(torch.int16)
+        o = torch.empty(rows, m.n_heads * m.head_dim, dtype=torch.int16, device=dev)
+        for _ in range(4):
+            sr.decode_attention(q, kp, vp, kt, vt, lt, o)
+        torch.cuda.synchronize()
+        del q, kp, vp, kt, vt, o
+        torch.cuda.empty_cache()
+        print(json.dumps({"case": "decode_attention", "rows": rows, "P": P, "lt": lt, "launches": 4}), flush=True)
+    if rm is not None and case in ("all", "rm"):
+        M = min(32768, cfg.n * cfg.tau)
+        x = torch.randn(M, m.d_model, device=dev).to(bf).view(torch.int16)
+        u = torch.randn(M, m.ffn_dim, device=dev).to(bf).view(torch.int16)
+        qkv_n = m.qkv_dim
+        for name, (xin, N, K, mode) in {"qkv": (x, qkv_n, m.d_model, 0), "o": (x, m.d_model, m.d_model, 1),
+                                        "w13": (x, m.ffn_dim, m.d_model, 2), "w2": (u, m.d_model, m.ffn_dim, 1)}.items():
+            w = (torch.randn(2 if mode == 2 else 1, N, K, device=dev) * 0.02).to(bf).view(torch.int16)
+            w = w if mode == 2 else w[0]
+            out = torch.zeros(M, N, device=dev, dtype=torch.int16 if mode in (2, 3) else torch.float32)
+            for _ in range(2):
+                sr.projection(xin, w, mode, out)
+            torch.cuda.synchronize()
+            print(json.dumps({"case": "rm_projection", "name": name, "M": M, "N": N, "K": K, "mode": mode,
+                              "launches": 2}), flush=True)
+            del w, out
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -179,6 +257,13 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--max-new-tokens", type=int, default=None,
                     help="shorter responses (for counter runs of the same kernels; not a bench line)")
+    ap.add_argument("--counter-workload", action="store_true",
+                    help="run the hot path's kernels at this configuration's shapes in short runs for rocprofv3 "
+                         "--pmc (see counter_workload) instead of the benchmark")
+    ap.add_argument("--counter-case", default="all", choices=["all", "decode", "attention", "rm"])
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run one elementwise kernel that reads 1 GiB and writes 1 GiB, so a counter run can "
+                         "scale FETCH_SIZE / WRITE_SIZE by what they read for a known byte count")
     ap.add_argument("--reward", choices=["model", "logprob"], default="model",
                     help="partial reward: the reward model, or the generator's mean log-probability "
                          "(section 5.3, no reward model)")
@@ -222,7 +307,18 @@ def main():
         rw = None   # the CPU leg runs the whole oracle only for small models
     torch.cuda.synchronize()
     log(f"[bench] weights uploaded ({time.time() - t:.1f}s)")
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
+        log("[bench] calibration kernel: 1 GiB read, 1 GiB written")
 
+    if args.counter_workload:
+        counter_workload(cfg, gen, rm, prompt, args.counter_case)
+        return
     rrc = 1 if args.reward_recompute else 0
     if args.memory_plan:
         free, _ = torch.cuda.mem_get_info()
