@@ -805,6 +805,308 @@ decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
   }
 }
 
+// Decode attention of a group of R = 16 / G rows of one KV head, the shared
+// prefix attended once for the whole group (bf16, head_dim 64 or 128, MFMA).
+// The 16 MFMA columns are the group's R rows x G query heads, so a prefix
+// key block costs the same MFMAs as one row's tail block but serves R rows.
+// Work-group = (split, KV head, row group), NW = R WPR waves: wave w takes
+// an even share of the prefix blocks (all 16 columns) and one WPR-th of row
+// (w mod R)'s tail blocks (its G columns are the ones kept); both runs
+// stream as in decode_wave_kernel (K into registers, V copied to the wave's
+// LDS double buffer and read back transposed).  The waves' prefix partials
+// and tail partials are merged per column through LDS; the work-group
+// writes the output or, with several splits, its partial slot.  Fused QKV
+// finalize: the wave holding a row's last tail block writes the row's
+// newest K/V first.
+template <int HD, int G, int WPR>
+__global__ void __launch_bounds__(64 * (16 / G) * WPR)
+decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
+                    int P, bf16_t* ktail, bf16_t* vtail, int cap, int lt, int hq, int hkv, int rows, int splits,
+                    float* __restrict__ part, bf16_t* __restrict__ out, float qscale, const float* __restrict__ qpart,
+                    int qsplits, int qkv_dim, const float2* __restrict__ rope) {
+  constexpr int R = 16 / G;             // rows per group
+  constexpr int NW = R * WPR;           // waves
+  constexpr int KS = HD / 32, DT = HD / 16, CPK = HD / 8;
+  constexpr int VB = 32 * HD;
+  constexpr int NDMA = VB * 2 / 1024;
+  constexpr int KPD = 64 / CPK;
+  constexpr int INFLIGHT = 2 * KS + NDMA;
+  static_assert(HD == 64 || HD == 128, "head_dim");
+  static_assert(G == 2 || G == 4 || G == 8, "query heads per KV head");
+  static_assert(NW <= 8 && NW * (16 + G) * (HD + 2) * 4 <= NW * 2 * VB * 2, "merge area within the V buffers");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NW * 2 * VB];
+  const int split = blockIdx.x, h = blockIdx.y, grp = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int fr = lane & 15, fg = lane >> 4;
+  const int rr = wave % R, wpart = wave / R;
+  const int row = grp * R + rr;                 // this wave's tail row
+  const bool rowvalid = row < rows;
+  // blocks: prefix [pb0, pb1) over all splits x waves; tail [tb0, tb1) of the row
+  const int nbp = (P + 31) >> 5, nbt = (lt + 31) >> 5;
+  const int pi = split * NW + wave, pn = splits * NW;
+  const int pb0 = nbp * pi / pn, pb1 = nbp * (pi + 1) / pn;
+  const int ti = split * WPR + wpart, tn = splits * WPR;
+  const int tb0 = rowvalid ? nbt * ti / tn : 0, tb1 = rowvalid ? nbt * (ti + 1) / tn : 0;
+  const bf16_t* kt = ktail + ((int64_t)(rowvalid ? row : 0) * hkv + h) * cap * HD;
+  const bf16_t* vt = vtail + ((int64_t)(rowvalid ? row : 0) * hkv + h) * cap * HD;
+  const bf16_t* kp = kpre + (int64_t)h * P * HD;
+  const bf16_t* vp = vpre + (int64_t)h * P * HD;
+  bf16_t* vbuf = lds + wave * 2 * VB;
+
+  // fused QKV finalize: the newest key's K (rotated) and V row of this row
+  const bool writer = qpart && rowvalid && lt > 0 && tb1 == nbt && tb1 > tb0;
+  if (writer) {
+    const int64_t qs = (int64_t)rows * qkv_dim;
+    const float* pk = qpart + (int64_t)row * qkv_dim + (hq + h) * HD;
+    const float* pv = pk + hkv * HD;
+    const int64_t at = (((int64_t)row * hkv + h) * cap + lt - 1) * HD;
+    for (int d = lane; d < HD / 2; d += 64) {
+      float k1v = 0.f, k2v = 0.f, v1 = 0.f, v2 = 0.f;
+      for (int sp = 0; sp < qsplits; ++sp) {
+        k1v += pk[sp * qs + d];
+        k2v += pk[sp * qs + HD / 2 + d];
+        v1 += pv[sp * qs + d];
+        v2 += pv[sp * qs + HD / 2 + d];
+      }
+      const float2 c = rope[d];
+      ktail[at + d] = f32_to_bf16(k1v * c.x - k2v * c.y);
+      ktail[at + HD / 2 + d] = f32_to_bf16(k2v * c.x + k1v * c.y);
+      vtail[at + d] = f32_to_bf16(v1);
+      vtail[at + HD / 2 + d] = f32_to_bf16(v2);
+    }
+    vm_wait<0>();
+  }
+
+  // Q^T (B operand): column fr = row grp R + fr / G, query head h G + fr % G
+  bf16x8 qf[KS];
+  {
+    const int qrow = grp * R + fr / G;
+    const bool qvalid = qrow < rows;
+    const int qr = qvalid ? qrow : 0, qh = h * G + fr % G;
+    float x[KS][8];
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[st][e] = 0.f;
+    if (qpart) {
+      const int64_t qs = (int64_t)rows * qkv_dim;
+      const float* pq = qpart + (int64_t)qr * qkv_dim + qh * HD + 8 * fg;
+      if (qvalid)
+        for (int sp = 0; sp < qsplits; ++sp) {
+#pragma unroll
+          for (int st = 0; st < KS; ++st) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(pq + sp * qs + 32 * st);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(pq + sp * qs + 32 * st + 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              x[st][e] += a[e];
+              x[st][4 + e] += b[e];
+            }
+          }
+        }
+#pragma unroll
+      for (int st = 0; st < KS / 2; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int d = 32 * st + 8 * fg + e;
+          const float x1 = x[st][e], x2 = x[st + KS / 2][e];
+          const float2 c = rope[d];
+          x[st][e] = x1 * c.x - x2 * c.y;
+          x[st + KS / 2][e] = x2 * c.x + x1 * c.y;
+        }
+    } else if (qvalid) {
+      const float* qp = q + ((int64_t)qr * hq + qh) * HD;
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[st][e] = qp[32 * st + 8 * fg + e];
+    }
+#pragma unroll
+    for (int st = 0; st < KS; ++st)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qf[st][e] = (__bf16)(qvalid ? x[st][e] * qscale : 0.f);
+  }
+
+  // block b of a run: keys [b0 + 32 b, min(b0 + 32 b + 32, b1)) of (kb, vb)
+  auto load_k = [&](const bf16_t* kb_, int k0, int k1, uint4 (&kr)[2][KS]) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int j = min(k0 + 16 * t + fr, k1 - 1);
+      const bf16_t* src = kb_ + (int64_t)j * HD;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) kr[t][st] = *reinterpret_cast<const uint4*>(src + 32 * st + 8 * fg);
+    }
+  };
+  auto copy_v = [&](const bf16_t* vb_, int k0, int k1, int buf) {
+    bf16_t* dst = vbuf + buf * VB;
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+      const int kk = i * KPD + lane / CPK;
+      const int c = vslot<CPK>(kk, lane % CPK);
+      const int j = min(k0 + kk, k1 - 1);
+      dma16(reinterpret_cast<const char*>(vb_ + (int64_t)j * HD + 8 * c), dst + i * 512);
+    }
+  };
+  const int kr0 = 4 * fg + (fr >> 2), kr1 = kr0 + 16;
+  auto compute = [&](int k0, int k1, const uint4 (&kr)[2][KS], int buf, f32x4 (&o)[DT], float& m, float& l) {
+    f32x4 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s2 = 0; s2 < KS; ++s2)
+        st[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[t][s2]), qf[s2], st[t], 0, 0,
+                                                        0);
+    }
+    const int jb = k0 + 4 * fg;
+    float sv[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sv[i] = jb + i < k1 ? st[0][i] : -INFINITY;
+      sv[4 + i] = jb + 16 + i < k1 ? st[1][i] : -INFINITY;
+    }
+    float mt = sv[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sv[i]);
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m, mt);
+    const bool none = mn == -INFINITY;
+    const float corr = none ? 1.f : exp2f(m - mn);
+    bf16x8 pf;
+    float ps = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float pv = none ? 0.f : exp2f(sv[i] - mn);
+      ps += pv;
+      pf[i] = (__bf16)pv;
+    }
+    l = l * corr + ps;
+    m = mn;
+    const bf16_t* vs = vbuf + buf * VB;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int c = 2 * dt + ((fr & 3) >> 1), e4 = 4 * (fr & 1);
+      const i16x4 lo = lds_read_tr16(vs + kr0 * HD + 8 * vslot<CPK>(kr0, c) + e4);
+      const i16x4 hi = lds_read_tr16(vs + kr1 * HD + 8 * vslot<CPK>(kr1, c) + e4);
+      o[dt] *= corr;
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tr16_pair(lo, hi), pf, o[dt], 0, 0, 0);
+    }
+  };
+  // one run of nb blocks starting at key b0 (block ends clamped to b1),
+  // the next block's loads in flight while a block is computed
+  auto run = [&](const bf16_t* kb_, const bf16_t* vb_, int b0, int b1, f32x4 (&o)[DT], float& m, float& l) {
+    const int nb = (b1 - b0 + 31) >> 5;
+    if (nb <= 0) return;
+    uint4 ka[2][KS], kb[2][KS];
+    load_k(kb_, b0, min(b0 + 32, b1), ka);
+    copy_v(vb_, b0, min(b0 + 32, b1), 0);
+    for (int b = 0; b < nb; b += 2) {
+      const int s0 = b0 + 32 * b, s1 = s0 + 32, s2 = s0 + 64;
+      if (b + 1 < nb) {
+        load_k(kb_, s1, min(s1 + 32, b1), kb);
+        copy_v(vb_, s1, min(s1 + 32, b1), 1);
+        vm_wait<INFLIGHT>();
+      } else {
+        vm_wait<0>();
+      }
+      compute(s0, min(s0 + 32, b1), ka, 0, o, m, l);
+      if (b + 1 < nb) {
+        asm volatile("" ::: "memory");
+        if (b + 2 < nb) {
+          load_k(kb_, s2, min(s2 + 32, b1), ka);
+          copy_v(vb_, s2, min(s2 + 32, b1), 0);
+          vm_wait<INFLIGHT>();
+        } else {
+          vm_wait<0>();
+        }
+        compute(s1, min(s1 + 32, b1), kb, 1, o, m, l);
+        asm volatile("" ::: "memory");
+      }
+    }
+  };
+
+  f32x4 op[DT], ot[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) op[dt] = ot[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mp = -INFINITY, lp = 0.f, mtl = -INFINITY, ltl = 0.f;
+  run(kp, vp, 32 * pb0, min(32 * pb1, P), op, mp, lp);
+  run(kt, vt, 32 * tb0, min(32 * tb1, lt), ot, mtl, ltl);
+
+  // merge: per column c (row grp R + c / G, head h G + c % G) the prefix
+  // partials of all waves and the tail partials of the row's WPR waves
+  lp += __shfl_xor(lp, 16, 64);
+  lp += __shfl_xor(lp, 32, 64);
+  ltl += __shfl_xor(ltl, 16, 64);
+  ltl += __shfl_xor(ltl, 32, 64);
+  __syncthreads();
+  constexpr int SL = HD + 2;
+  float* sp_ = reinterpret_cast<float*>(lds);   // [NW][16][SL] prefix partials
+  float* st_ = sp_ + NW * 16 * SL;               // [NW][G][SL] tail partials (the wave's row)
+  {
+    float* w = sp_ + (wave * 16 + fr) * SL;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[dt * 16 + 4 * fg + i] = op[dt][i];
+    if (fg == 0) {
+      w[HD] = mp;
+      w[HD + 1] = lp;
+    }
+    if (fr / G == rr) {
+      float* wt = st_ + (wave * G + fr % G) * SL;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) wt[dt * 16 + 4 * fg + i] = ot[dt][i];
+      if (fg == 0) {
+        wt[HD] = mtl;
+        wt[HD + 1] = ltl;
+      }
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 16 * HD; idx += 64 * NW) {
+    const int c = idx / HD, d = idx % HD;
+    const int orow = grp * R + c / G, g = c % G;
+    if (orow >= rows) continue;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sp_[(w * 16 + c) * SL + HD]);
+#pragma unroll
+    for (int w = c / G; w < NW; w += R) M = fmaxf(M, st_[(w * G + g) * SL + HD]);
+    float L = 0.f, A = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float* ws = sp_ + (w * 16 + c) * SL;
+        const float cf = exp2_or_zero(ws[HD] - M);
+        L += ws[HD + 1] * cf;
+        A += ws[d] * cf;
+      }
+#pragma unroll
+      for (int w = c / G; w < NW; w += R) {
+        const float* ws = st_ + (w * G + g) * SL;
+        const float cf = exp2_or_zero(ws[HD] - M);
+        L += ws[HD + 1] * cf;
+        A += ws[d] * cf;
+      }
+    }
+    const int qh = h * G + g;
+    if (splits == 1) {
+      out[((int64_t)orow * hq + qh) * HD + d] = f32_to_bf16(A / L);
+    } else {
+      float* pp = part + (((int64_t)orow * hq + qh) * splits + split) * (HD + 2);
+      pp[d] = A;
+      if (d == 0) {
+        pp[HD] = M;
+        pp[HD + 1] = L;
+      }
+    }
+  }
+}
+
 template <typename T, int HD>
 __global__ void decode_merge_kernel(const float* __restrict__ part, int splits, T* __restrict__ out) {
   const int rq = blockIdx.x;  // row * hq + qh
@@ -927,6 +1229,41 @@ static bool wave_form(int dtype, int hd, int g) {
   return dtype == SR_BF16 && (hd == 64 || hd == 128) && (g == 1 || g == 2 || g == 4 || g == 8);
 }
 
+// Whether decode_group_kernel takes the launch: bf16, head_dim 64 or 128, 2,
+// 4 or 8 query heads per KV head, a prefix, and from 64 rows (fewer rows
+// give too few work-groups without splitting).  Waves per row: two where
+// that stays within about kWaveTarget waves (not for 2 query heads per KV
+// head: eight rows a group already make eight waves), else one.
+constexpr int kGroupMinRows = 64;
+static bool group_form(int dtype, int hd, int g, int P, int rows) {
+  return dtype == SR_BF16 && (hd == 64 || hd == 128) && (g == 2 || g == 4 || g == 8) && P > 0 &&
+         rows >= kGroupMinRows;
+}
+static int group_wpr(int g, int rows, int hkv) {
+  const int R = 16 / g;
+  const int64_t waves1 = (int64_t)((rows + R - 1) / R) * hkv * R;
+  return (g != 2 && waves1 * 2 <= kWaveTarget + kWaveTarget / 8) ? 2 : 1;
+}
+
+template <int HD, int G>
+static void launch_group(const DecodeAttnArgs& a, float qscale, hipStream_t s) {
+  constexpr int R = 16 / G;
+  const int wpr = group_wpr(G, a.rows, a.hkv);
+  dim3 grid(1, a.hkv, (a.rows + R - 1) / R);
+#define SR_GROUP(W)                                                                                               \
+  hipLaunchKernelGGL((decode_group_kernel<HD, G, W>), grid, dim3(64 * R * W), 0, s, a.q, (const bf16_t*)a.kpre,  \
+                     (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv,   \
+                     a.rows, 1, a.part, (bf16_t*)a.out, qscale, a.qpart, a.qsplits, a.qkv_dim, a.rope)
+  if constexpr (G != 2) {
+    if (wpr == 2) SR_GROUP(2);
+    else SR_GROUP(1);
+  } else {
+    SR_GROUP(1);
+  }
+#undef SR_GROUP
+  SR_CHECK_LAUNCH();
+}
+
 template <int HD, int G>
 static void launch_wave(const DecodeAttnArgs& a, int key0, const WavePlan& w, bool direct, float qscale,
                         hipStream_t s) {
@@ -955,6 +1292,14 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
                        a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
     SR_CHECK_LAUNCH();
   };
+  if constexpr ((HD == 64 || HD == 128) && (G == 2 || G == 4 || G == 8)) {
+    if (group_form(a.dtype, HD, G, a.P, a.rows)) {
+      SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), SR_ERR_INTERNAL,
+                 "fused QKV finalize needs a new key");
+      launch_group<HD, G>(a, qscale, s);
+      return;
+    }
+  }
   if constexpr (HD == 64 || HD == 128) {
     if (wave_form(a.dtype, HD, G)) {
       // the key-split kernel over the keys past the prefix pass's, then the
@@ -1091,6 +1436,7 @@ size_t decode_attn_part_floats(const DecodeAttnArgs& a) {
   if (a.rows <= 0 || a.hkv <= 0 || a.hq % a.hkv) return 0;
   const int g = a.hq / a.hkv;
   const size_t per = (size_t)a.rows * a.hq * (a.hd + 2);
+  if (group_form(a.dtype, a.hd, g, a.P, a.rows)) return 0;
   if (wave_form(a.dtype, a.hd, g)) {
     const bool pre = prefix_by_mfma(a.dtype, a.hd, a.P, a.rows);
     const int keys = a.P + a.lt - (pre ? a.P : 0);

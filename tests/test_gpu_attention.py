@@ -47,6 +47,13 @@ CASES = [
     ("bf16", 128, 16, 2, 9, 64, 130, 130),
     ("bf16", 64, 32, 8, 33, 256, 129, 130),
     ("bf16", 64, 8, 2, 7, 128, 33, 40),
+    # row groups sharing the prefix: head_dim 64 at the 1B run's rows, four
+    # and eight query heads per KV head, a partial last group
+    ("bf16", 64, 32, 8, 256, 256, 129, 130),
+    ("bf16", 64, 32, 8, 66, 256, 500, 512),
+    ("bf16", 64, 8, 2, 64, 128, 33, 40),
+    ("bf16", 128, 64, 8, 101, 256, 77, 80),
+    ("bf16", 128, 32, 8, 64, 33, 1, 8),
     ("f32", 32, 4, 4, 16, 32, 17, 64),
     ("f32", 32, 8, 1, 6, 5, 3, 3),
 ]

@@ -59,12 +59,14 @@ def test_noalloc_rejects_partials_beyond_the_static_scratch():
     torch, sr = need_gpu()
     limit = sr.decode_attention_noalloc_limit()
     assert limit == 32 << 20
-    # 2100 rows of 32 query heads: one partial slot of 130 floats per row and
-    # head for the prefix pass to fold in, 8.7 M floats > 8 M
+    # 2100 rows of 32 query heads, one per KV head (the row groups that share
+    # the prefix take 2, 4 or 8 query heads per KV head): one partial slot of
+    # 130 floats per row and head for the prefix pass to fold in, 8.7 M
+    # floats > 8 M
     rows, P, lt, cap = 2100, 256, 9, 16
     q = torch.zeros((rows, 32, 128), dtype=torch.float32, device="cuda")
-    kp = torch.zeros((8, P, 128), dtype=torch.int16, device="cuda")
-    kt = torch.zeros((rows, 8, cap, 128), dtype=torch.int16, device="cuda")
+    kp = torch.zeros((32, P, 128), dtype=torch.int16, device="cuda")
+    kt = torch.zeros((rows, 32, cap, 128), dtype=torch.int16, device="cuda")
     out = torch.zeros((rows, 32 * 128), dtype=torch.int16, device="cuda")
     with pytest.raises(sr.SpecRejError) as e:
         sr.decode_attention_noalloc(q, kp, kp, kt, kt, lt, out)
