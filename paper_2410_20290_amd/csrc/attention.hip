@@ -2,15 +2,23 @@
 //
 // Decode: every candidate row has one query (the newest token).  Keys are
 // the prompt prefix, stored once and shared by all rows, followed by the
-// row's own tail.  A work-group owns (row, KV head, key split) and serves the
-// whole query-head group of that KV head, so each K/V byte is read once per
-// row.  16-byte loads; lanes of one key row are adjacent, so a wave reads
-// whole contiguous rows.  Online softmax in base 2; split partials are merged
-// by log-sum-exp in a second kernel.
+// row's own tail.  The query heads of one KV head are the columns of a
+// v_mfma_f32_16x16x32_bf16 (S^T = K Q^T, O^T += V^T P^T), so each K/V byte is
+// read once per row, and once per group of 16 / G rows for the prefix:
+//   decode_group_kernel  (bf16, 64+ rows): a work-group takes a row group;
+//                        its waves share the prefix blocks and split the
+//                        rows' tails;
+//   decode_wave_kernel   (bf16, fewer rows or no prefix): a work-group takes
+//                        one (row, KV head), its waves split the keys;
+//   decode_attn_kernel   (fp32 and head_dim 32): vector ALU, 16-byte loads,
+//                        DPP reductions;
+//   prefill_attn_mfma_kernel<.., true>: the prefix of 16 rows at once, for
+//                        the one-query-head-per-KV-head case at 128+ rows.
+// Online softmax in base 2; split partials are merged by log-sum-exp.
 //
-// Prefill (reward-model scoring, prompt): a work-group owns a block of
-// queries of one row and one KV head; K/V tiles are staged in LDS as fp32
-// and shared by all its queries.
+// Prefill (reward-model scoring, prompt): a work-group owns 16 queries of
+// one row and one KV head (MFMA flash attention, bf16 head_dim 64/128), or a
+// block of queries on the vector ALU with K/V staged in LDS as fp32.
 #include <algorithm>
 #include <mutex>
 
@@ -232,270 +240,6 @@ decode_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, cons
   }
 }
 
-// Wait until at most N vector-memory operations of this wave are in flight,
-// then meet the other waves.
-template <int N>
-__device__ __forceinline__ void tail_stage_wait() {
-  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  else static_assert(N < 0, "add this wait count");
-}
-
-// Decode attention over keys [key0, P + lt) for bf16, head_dim 128, on
-// MFMA.  Work-group = (split, KV head, row), 4 waves; the G query heads of
-// the KV head are the 16 columns of v_mfma_f32_16x16x32_bf16 (columns >= G
-// are zero queries whose results are dropped).  Stage = SK keys of K and V
-// (SK / 2 KB) copied into LDS with global_load_lds_dwordx4, NST - 1 stages
-// ahead.
-// Per 32 keys every wave computes
-//   S^T = K Q^T   (two 16-key tiles): lane l holds keys 4(l/16)+i and
-//                 16+4(l/16)+i of query l%16 (all waves alike),
-// the online-softmax update (maximum over the four lane groups), and
-//   O^T += V^T P^T for its own 32 of the 128 dimensions, with the key order
-//                 of the contraction permuted so that the B operand is the
-//                 lane's own 8 probabilities; the A operand reads V at those
-//                 keys (2-byte LDS reads of one dimension).
-// LDS rows of 256 bytes (16 chunks of 8 dims): K chunk c of key k sits in
-// slot c ^ (k & 15), V chunk c in slot c ^ 2 ((k >> 2) & 3), so both read
-// patterns are free of bank conflicts.
-template <int G, int SK, int NST>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SK == 32 ? 4 : 1)))
-decode_tail_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
-                        int P, bf16_t* ktail, bf16_t* vtail, int cap, int lt,
-                        int hq, int hkv, int kps, int splits, float* __restrict__ part, bf16_t* __restrict__ out,
-                        float qscale, int key0, int split0, const float* __restrict__ qpart, int qsplits,
-                        int qkv_dim, const float2* __restrict__ rope, float* __restrict__ qout) {
-  constexpr int HD = 128;
-  constexpr int STAGE = 2 * SK * HD;  // bf16 elements: K rows then V rows
-  constexpr int DI = SK / 16;         // DMA instructions per wave per stage, for K and again for V
-  static_assert(SK % 32 == 0 && NST >= 2, "stage shape");
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
-  const int split = blockIdx.x, h = blockIdx.y, row = blockIdx.z;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int fr = lane & 15, fg = lane >> 4;
-  const int total = P + lt;
-  const int k0 = key0 + split * kps, k1 = min(total, k0 + kps);
-  const int nst = (k1 - k0 + SK - 1) / SK;
-
-  // DMA: a stage is 32 instructions of 4 key rows (1 KB); wave w issues K
-  // rows 4 (w + 4 i) .. + 3, i < 4, and the same V rows.  Lane l writes slot
-  // l % 16 of row l / 16 and fetches the chunk stored there.
-  const bf16_t* kt = ktail + ((int64_t)row * hkv + h) * cap * HD;
-  const bf16_t* vt = vtail + ((int64_t)row * hkv + h) * cap * HD;
-  const bf16_t* kp = kpre + (int64_t)h * P * HD;
-  const bf16_t* vp = vpre + (int64_t)h * P * HD;
-  auto issue = [&](int st, int buf) {
-    bf16_t* dst = lds + buf * STAGE;
-#pragma unroll
-    for (int i = 0; i < DI; ++i) {
-      const int kr = 4 * (wave + 4 * i) + fg;  // key row in the stage
-      const int j = min(k0 + min(st, nst - 1) * SK + kr, k1 - 1);
-      const int64_t rowoff = (int64_t)(j < P ? j : j - P) * HD;
-      const int ck = fr ^ (kr & 15), cv = fr ^ (2 * ((kr >> 2) & 3));
-      dma16(reinterpret_cast<const char*>((j < P ? kp : kt) + rowoff + ck * 8), dst + (wave + 4 * i) * 512);
-      dma16(reinterpret_cast<const char*>((j < P ? vp : vt) + rowoff + cv * 8), dst + SK * HD + (wave + 4 * i) * 512);
-    }
-  };
-
-  // Fused QKV finalize.  The work-group that holds the newest key (response
-  // index lt - 1) writes its K (rotated) and V row first; vector-memory
-  // operations of a wave complete in issue order, so the wait before any
-  // later DMA of that row (the prologue's below, else a step's wait plus
-  // barrier) also covers these stores.
-  const bool writer = qpart && k1 == total;
-  if (writer && wave == 0) {
-    const int64_t qs = (int64_t)gridDim.z * qkv_dim;
-    const float* pk = qpart + (int64_t)row * qkv_dim + (hq + h) * HD;
-    const float* pv = pk + hkv * HD;
-    float k1v = 0.f, k2v = 0.f, v1 = 0.f, v2 = 0.f;
-    for (int sp = 0; sp < qsplits; ++sp) {
-      k1v += pk[sp * qs + lane];
-      k2v += pk[sp * qs + 64 + lane];
-      v1 += pv[sp * qs + lane];
-      v2 += pv[sp * qs + 64 + lane];
-    }
-    const float2 c = rope[lane];
-    const int64_t at = (((int64_t)row * hkv + h) * cap + lt - 1) * HD;
-    ktail[at + lane] = f32_to_bf16(k1v * c.x - k2v * c.y);
-    ktail[at + 64 + lane] = f32_to_bf16(k2v * c.x + k1v * c.y);
-    vtail[at + lane] = f32_to_bf16(v1);
-    vtail[at + 64 + lane] = f32_to_bf16(v2);
-  }
-  if (writer && nst - 1 <= NST - 2) {
-    // the newest key is in a prologue stage
-    if (wave == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-  }
-  f32x4 o[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-  float m = -INFINITY, l = 0.f;
-  // V^T reads: dimension 32 wave + 16 dt + fr, keys 4 fg + i (+ 16)
-  const int vdim0 = 32 * wave + fr;
-
-  // stages 0 .. NST - 2 ahead; every step then refills the buffer of the
-  // step before.  The 32-key form fetches only stages that exist (a copy
-  // past the last stage would hold the work-group at its final wait for a
-  // round trip); the 64-key form fetches the last stage again instead, which
-  // keeps its loop's code as compiled before (measured 0.2-1 us faster per
-  // launch at 21 rows than with the skip).
-  constexpr bool SKIP = SK == 32;
-#pragma unroll
-  for (int st = 0; st < NST - 1; ++st)
-    if (!SKIP || st < nst) issue(st, st);
-
-  // Q^T fragments (B operand): lane holds Q[query fr][32 s + 8 fg .. + 8],
-  // scaled, bf16; loaded under the prologue's DMAs.  Fused: the partials of
-  // dimensions d and d + 64 (a rotation pair) are the lane's s and s + 2.
-  bf16x8 qf[4];
-  {
-    const bool qvalid = fr < G;
-    const int qh = h * G + (qvalid ? fr : 0);
-    if (qpart) {
-      const int64_t qs = (int64_t)gridDim.z * qkv_dim;
-      const float* pq = qpart + (int64_t)row * qkv_dim + qh * HD + 8 * fg;
-      f32x4 x[2][2][2];  // [s][half][four of eight]
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int f = 0; f < 2; ++f) x[s][hf][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (qvalid)
-        for (int sp = 0; sp < qsplits; ++sp) {
-          f32x4 y[2][2][2];
-#pragma unroll
-          for (int s = 0; s < 2; ++s)
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-              for (int f = 0; f < 2; ++f)
-                y[s][hf][f] = *reinterpret_cast<const f32x4*>(pq + sp * qs + 64 * hf + 32 * s + 4 * f);
-#pragma unroll
-          for (int s = 0; s < 2; ++s)
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-              for (int f = 0; f < 2; ++f) x[s][hf][f] += y[s][hf][f];
-        }
-      float* qo = qout && split == 0 && wave == 0 && qvalid ? qout + ((int64_t)row * hq + qh) * HD : nullptr;
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int d = 32 * s + 8 * fg + e;
-          const float x1 = x[s][0][e >> 2][e & 3], x2 = x[s][1][e >> 2][e & 3];
-          const float2 c = rope[d];
-          const float y1 = x1 * c.x - x2 * c.y, y2 = x2 * c.x + x1 * c.y;
-          qf[s][e] = (__bf16)(qvalid ? y1 * qscale : 0.f);
-          qf[s + 2][e] = (__bf16)(qvalid ? y2 * qscale : 0.f);
-          if (qo) {
-            qo[d] = y1;
-            qo[64 + d] = y2;
-          }
-        }
-    } else {
-      const float* qr = q + ((int64_t)row * hq + qh) * HD;
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qf[s][e] = (__bf16)(qvalid ? qr[32 * s + 8 * fg + e] * qscale : 0.f);
-    }
-  }
-  int cur = 0;  // buffer of step t
-  for (int t = 0; t < nst; ++t) {
-    // all but the copies of the NST - 2 stages after t while those were all
-    // issued; near the end (when skipping) every copy
-    if (!SKIP || t + NST - 2 < nst) tail_stage_wait<(NST - 2) * 2 * DI>();
-    else tail_stage_wait<0>();
-    if (!SKIP || t + NST - 1 < nst) issue(t + NST - 1, cur == 0 ? NST - 1 : cur - 1);
-    const bf16_t* ks = lds + cur * STAGE;
-    const bf16_t* vs = ks + SK * HD;
-    cur = cur == NST - 1 ? 0 : cur + 1;
-#pragma unroll
-    for (int tp = 0; tp < SK / 32; ++tp) {
-      f32x4 st[2];
-#pragma unroll
-      for (int kt2 = 0; kt2 < 2; ++kt2) {
-        const int key = 32 * tp + 16 * kt2 + fr;
-        st[kt2] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + key * HD + 8 * ((4 * s + fg) ^ (key & 15)));
-          st[kt2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[kt2], 0, 0, 0);
-        }
-      }
-      // this lane's 8 keys: 4 fg + i and 16 + 4 fg + i of the 32
-      float sv[8];
-      const int jb = k0 + t * SK + 32 * tp + 4 * fg;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sv[i] = jb + i < k1 ? st[0][i] : -INFINITY;
-        sv[4 + i] = jb + 16 + i < k1 ? st[1][i] : -INFINITY;
-      }
-      float mt = sv[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) mt = fmaxf(mt, sv[i]);
-      mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float mn = fmaxf(m, mt);
-      const bool none = mn == -INFINITY;
-      const float corr = none ? 1.f : exp2f(m - mn);
-      bf16x8 pf;
-      float ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float p = none ? 0.f : exp2f(sv[i] - mn);
-        ps += p;
-        pf[i] = (__bf16)p;
-      }
-      l = l * corr + ps;
-      m = mn;
-#pragma unroll
-      for (int dt = 0; dt < 2; ++dt) {
-        const int dim = vdim0 + 16 * dt;
-        const int dc = dim >> 3, de = dim & 7;
-        bf16x8 vf;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int key = 32 * tp + 4 * fg + (i & 3) + 16 * (i >> 2);
-          vf[i] = __builtin_bit_cast(__bf16, vs[key * HD + 8 * (dc ^ (2 * ((key >> 2) & 3))) + de]);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[dt][e] *= corr;
-        o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[dt], 0, 0, 0);
-      }
-    }
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-  // the row sum over the four lane groups; lane l now holds O^T[dims
-  // 32 w + 16 dt + 4 fg + e][query fr]
-  l += __shfl_xor(l, 16, 64);
-  l += __shfl_xor(l, 32, 64);
-  if (fr < G) {
-    const int qh = h * G + fr;
-#pragma unroll
-    for (int dt = 0; dt < 2; ++dt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int dim = 32 * wave + 16 * dt + 4 * fg + e;
-        if (out) {
-          out[((int64_t)row * hq + qh) * HD + dim] = f32_to_bf16(o[dt][e] / l);
-        } else {
-          float* pp = part + (((int64_t)row * hq + qh) * splits + split0 + split) * (HD + 2);
-          pp[dim] = o[dt][e];
-          if (wave == 0 && dt == 0 && fg == 0 && e == 0) {
-            pp[HD] = m;
-            pp[HD + 1] = l;
-          }
-        }
-      }
-  }
-}
-
 // ------------------------------------------------ decode (waves split keys)
 // Wait until at most N vector-memory operations of this wave are in flight.
 template <int N>
@@ -534,8 +278,10 @@ __device__ __forceinline__ int vslot(int k, int c) {
 // computed.  Online softmax in base 2 (q carries log2 e / sqrt(hd)).  The
 // waves' (max, sum, unnormalised output) are merged through LDS; the
 // work-group writes the output or, with several splits, its partial slot.
-// Fused QKV finalize as in decode_tail_mfma_kernel: the wave that holds the
-// newest key writes its K (rotated) and V row before it loads any key.
+// Fused QKV finalize (the decode step's QKV projection leaves split-K
+// partials): q is summed from them and rotated here, and the wave that holds
+// the newest key sums, rotates and writes its K and V row before it loads
+// any key.
 template <int HD, int G, int NW>
 __global__ void __launch_bounds__(64 * NW)
 decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
@@ -1136,17 +882,6 @@ static int decode_kps(int rows, int hkv, int keys) {
 // Waves decode_wave_kernel aims at over the whole grid.
 constexpr int kWaveTarget = 2048;
 
-// Keys per split for the MFMA streaming kernel: as many splits as keep the
-// grid within one round of resident work-groups (two per CU), at least 64
-// keys per split (a partly filled second round measured slower).
-static int tail_mfma_kps(int rows, int hkv, int keys) {
-  constexpr int target = 512;
-  const int64_t groups = (int64_t)rows * hkv;
-  int splits = (int)std::max<int64_t>(1, target / groups);
-  splits = std::max(1, std::min(splits, keys / 64));
-  return (keys + splits - 1) / splits;
-}
-
 template <int HD, int G, bool PREFIX_ONLY>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
@@ -1165,38 +900,11 @@ static bool prefix_by_mfma(int dtype, int hd, int P, int rows) {
 int decode_attn_splits(int rows, int hkv, int keys) {
   int kps = decode_kps(rows, hkv, keys);
   const int old_form = (keys + kps - 1) / kps + (keys + 63) / 64;
-  const int dma_form = keys > 0 ? (keys + tail_mfma_kps(rows, hkv, keys) - 1) / tail_mfma_kps(rows, hkv, keys) : 0;
   // the key-split kernel: splits <= the waves it wants per (row, KV head),
   // which grow with the key count
   const int64_t pairs = std::max<int64_t>(1, (int64_t)rows * hkv);
   const int wave_form_max = (int)std::max<int64_t>(1, std::min<int64_t>(kWaveTarget / pairs, (keys + 31) / 32));
-  return std::max({old_form, dma_form + (keys + 63) / 64, wave_form_max});
-}
-
-// Whether the MFMA streaming kernel takes the keys (bf16, head_dim 128, up to
-// 16 query heads per KV head, up to 1024 rows: measured faster than the
-// per-query kernel at 21, 103 and 512 rows).
-static bool tail_by_mfma(int dtype, int hd, int g, int rows) {
-  return dtype == SR_BF16 && hd == 128 && g <= 16 && rows <= 1024;
-}
-
-template <int G>
-static void launch_tail_mfma(const DecodeAttnArgs& a, int key0, int kps, int nsplit, int splits, int split0,
-                             float qscale, hipStream_t s) {
-#define SR_TAIL(SK, NST)                                                                                        \
-  hipLaunchKernelGGL((decode_tail_mfma_kernel<G, SK, NST>), dim3(nsplit, a.hkv, a.rows), dim3(256), 0, s, a.q, \
-                     (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail,      \
-                     a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part, (bf16_t*)a.out, qscale, key0, split0,        \
-                     a.qpart, a.qsplits, a.qkv_dim, a.rope, a.qout)
-  // 64-key stages hold 2 work-groups per CU (registers and LDS), 32-key
-  // stages 4: the latter when one work-group per (row, KV head) alone
-  // exceeds a round of the former (more resident waves to hide the
-  // dependent MFMA / softmax chain); the former, with fewer barriers per
-  // key, otherwise
-  if ((int64_t)a.rows * a.hkv > 2 * 256) SR_TAIL(32, 2);
-  else SR_TAIL(64, 2);
-#undef SR_TAIL
-  SR_CHECK_LAUNCH();
+  return std::max(old_form, wave_form_max);
 }
 
 // Work split of decode_wave_kernel over `keys` keys of rows x hkv (row, KV
@@ -1331,36 +1039,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
       return;
     }
   }
-  if (tail_by_mfma(a.dtype, HD, G, a.rows)) {
-    // the streaming kernel over the keys past the prefix pass's, then the
-    // prefix pass or (several splits without it) the merge
-    const bool pre = prefix_by_mfma(a.dtype, HD, a.P, a.rows);
-    SR_REQUIRE(!a.qpart || (a.lt >= 1 && a.rope && a.qsplits >= 1), SR_ERR_INTERNAL,
-               "fused QKV finalize needs a new key");
-    const int key0 = pre ? a.P : 0;
-    const int keys = a.P + a.lt - key0;
-    const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
-    const int tsplits = (keys + kps - 1) / kps;
-    const bool direct = !pre && tsplits == 1;
-    if (!direct)
-      SR_REQUIRE((size_t)a.rows * a.hq * std::max(tsplits, 1) * (HD + 2) <= a.part_cap, 5,
-                 "attention partial buffer too small");
-    if (tsplits > 0) {
-      DecodeAttnArgs b = a;
-      if (!direct) b.out = nullptr;
-      if (!pre) b.qout = nullptr;  // only the prefix pass reads q back
-      launch_tail_mfma<G>(b, key0, kps, tsplits, tsplits, 0, qscale, s);
-    }
-    if (pre) {
-      prefix_pass(tsplits);
-    } else if (!direct) {
-      hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, tsplits,
-                         (T*)a.out);
-      SR_CHECK_LAUNCH();
-    }
-    return;
-  }
-  SR_REQUIRE(!a.qpart, SR_ERR_INTERNAL, "fused QKV finalize without the streaming kernel");
+  SR_REQUIRE(!a.qpart, SR_ERR_INTERNAL, "fused QKV finalize without the MFMA decode kernels");
   if (prefix_by_mfma(a.dtype, HD, a.P, a.rows)) {
     // tail partials, then the prefix pass
     const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;
@@ -1421,7 +1100,7 @@ bool decode_attn_fuses_qkv(const DecodeAttnArgs& a) {
   if (a.hkv <= 0 || a.hq % a.hkv) return false;
   const int g = a.hq / a.hkv;
   return (g == 1 || g == 2 || g == 4 || g == 8) && a.lt >= 1 &&
-         (wave_form(a.dtype, a.hd, g) || tail_by_mfma(a.dtype, a.hd, g, a.rows));
+         wave_form(a.dtype, a.hd, g);
 }
 
 void decode_attn(const DecodeAttnArgs& a, hipStream_t s) {
@@ -1443,13 +1122,6 @@ size_t decode_attn_part_floats(const DecodeAttnArgs& a) {
     if (keys <= 0) return 0;
     const WavePlan w = wave_plan(a.rows, a.hkv, keys);
     return (!pre && w.splits == 1) ? 0 : per * w.splits;
-  }
-  if (a.dtype == SR_BF16 && a.hd == 128 && tail_by_mfma(a.dtype, a.hd, g, a.rows)) {
-    const bool pre = prefix_by_mfma(a.dtype, a.hd, a.P, a.rows);
-    const int keys = a.P + a.lt - (pre ? a.P : 0);
-    const int kps = keys > 0 ? tail_mfma_kps(a.rows, a.hkv, keys) : 1;
-    const int tsplits = (keys + kps - 1) / kps;
-    return (!pre && tsplits == 1) ? 0 : per * std::max(tsplits, 1);
   }
   if (prefix_by_mfma(a.dtype, a.hd, a.P, a.rows)) {
     const int tkps = a.lt > 0 ? decode_kps(a.rows, a.hkv, a.lt) : 1;

@@ -537,8 +537,11 @@ static void decode_step(const Ctx& c, const Model& G, const State& st, int rows,
                      cap, step - 1, c.s);
       });
     }
+    // the method's own attention bytes: the keys and values (the prefix
+    // once), the query and the output; the QKV split partials the fused
+    // finalize reads are the projection's traffic, not counted here
     const double abytes = 2.0 * m.hkv * m.hd * m.es * ((double)pl.P + (double)rows * step) +
-                          (double)rows * m.hq * m.hd * (4 + m.es) + (a.qpart ? qbytes : 0.0);
+                          (double)rows * m.hq * m.hd * (4 + m.es);
     const double aflops = 4.0 * rows * m.hq * m.hd * ((double)pl.P + step);
     timed(c, SR_K_DECODE_ATTN, abytes, aflops, [&] { decode_attn(a, c.s); });
     sp = run_gemm(c, true, m.dtype, L.o, m.hq * m.hd, G.wo(l), m.hq * m.hd, rows, m.d, m.hq * m.hd, EPI_PARTIAL,
