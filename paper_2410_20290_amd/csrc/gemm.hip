@@ -914,26 +914,86 @@ __device__ __forceinline__ void vm_barrier_ahead(int a) {
 // For the decode projections (a few hundred rows at most) the weights are
 // streamed once from HBM; what matters is keeping enough of them in flight
 // and keeping the per-step overhead small.  Block tile BM x BN (PAIRED: BN
-// gate rows then BN up rows, BN output columns), K step BK (64 or 128), NST
-// LDS stages filled by global_load_lds_dwordx4 up to NST - 1 steps ahead,
-// one barrier per step.  LDS stage: the BM activation rows then the weight
-// rows, 2 BK bytes each; 16-byte chunk c of row r sits in slot c ^ (r & 15)
-// (BK 128) or c ^ (r & 7) ^ ((r >> 3) & 1) (BK 64), so the fragment reads of
-// 16 consecutive rows are free of bank conflicts.  4 waves in a WGM x WGN
+// gate rows then BN up rows, BN output columns), K step BK (64, 128 or
+// 256), NST LDS stages filled by global_load_lds_dwordx4 up to NST - 1 steps
+// ahead, one barrier per step.  LDS stage: the BM activation rows then the
+// weight rows, 2 BK bytes each; 16-byte chunk c of row r sits in slot
+// c ^ (r & 15) (BK 128, 256) or c ^ (r & 7) ^ ((r >> 3) & 1) (BK 64), so the
+// fragment reads of 16 consecutive rows are free of bank conflicts.  With
+// rot > 0 tile n visits its K steps from step (n rot) mod nk on, wrapping
+// around (the same products, summed in that order).  4 waves in a WGM x WGN
 // grid, each a (BM / WGM) x (BN / WGN) tile of v_mfma_f32_16x16x32_bf16
 // accumulators; the fragment reads of the next 32-wide sub-step run under
 // the MFMAs of the current one.
 
 template <int BK>
 __device__ __forceinline__ int stream_slot(int c, int r) {
-  if constexpr (BK == 128) return c ^ (r & 15);
+  if constexpr (BK >= 128) return c ^ (r & 15);
   else return c ^ (r & 7) ^ ((r >> 3) & 1);
+}
+
+// Epilogue of the few-row kernels.  The weight fragment is the first MFMA
+// operand, so the accumulators hold the transposed tile: lane l has row
+// mrow + 16 i and the four consecutive columns ncol + 16 j .. + 3, stored as
+// one 16-byte (fp32) or 8-byte (bf16) chunk where the row is aligned and the
+// columns are inside the output.
+template <int NB, int TI, int TJ, bool PAIRED>
+__device__ __forceinline__ void stream_epilogue(const f32x4 (&acc)[NB][TI][TJ], int mrow, int ncol, int M, int N,
+                                                int split, const EpiArgs& epi, float* __restrict__ partial) {
+  const bool to_part = partial != nullptr;
+  const bool resid = !PAIRED && !to_part && epi.mode == EPI_RESID;
+  const bool bf = !to_part && !resid && epi.out_bf16;
+  const int64_t ld = to_part ? (int64_t)NB * N : (int64_t)epi.ldo;
+  const bool aligned = to_part ? (N % 4 == 0 && (reinterpret_cast<uintptr_t>(partial) & 15) == 0)
+                               : (epi.ldo % 4 == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0);
+  float* const fbase = to_part ? partial + (int64_t)split * M * ld : reinterpret_cast<float*>(epi.out);
+  bf16_t* const bbase = reinterpret_cast<bf16_t*>(epi.out);
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const int m = mrow + 16 * i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int n = ncol + 16 * j;
+      if (n >= N) continue;
+      const bool full = aligned && n + 3 < N;
+      const int64_t off = (int64_t)m * ld + n;
+      f32x4 v = acc[0][i][j];
+      if (to_part) {
+        if (full) {
+          store4(fbase + off, v);
+          if (PAIRED) store4(fbase + off + N, acc[NB - 1][i][j]);
+        } else {
+          for (int k = 0; k < 4 && n + k < N; ++k) {
+            fbase[off + k] = v[k];
+            if (PAIRED) fbase[off + N + k] = acc[NB - 1][i][j][k];
+          }
+        }
+        continue;
+      }
+      if (PAIRED) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = silu(v[k]) * acc[NB - 1][i][j][k];
+      }
+      if (full) {
+        if (resid) v += *reinterpret_cast<const f32x4*>(fbase + off);
+        if (bf) store4(bbase + off, v);
+        else store4(fbase + off, v);
+      } else {
+        for (int k = 0; k < 4 && n + k < N; ++k) {
+          if (resid) fbase[off + k] += v[k];
+          else if (bf) bbase[off + k] = f32_to_bf16(v[k]);
+          else fbase[off + k] = v[k];
+        }
+      }
+    }
+  }
 }
 
 template <int BM, int BN, int WGM, int WGN, int NST, bool PAIRED, int BK>
 __global__ void __launch_bounds__(256)
 gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb,
-                   int64_t pair_off, int M, int N, int K, int k_per_split, EpiArgs epi,
+                   int64_t pair_off, int M, int N, int K, int k_per_split, int rot, EpiArgs epi,
                    float* __restrict__ partial) {
   constexpr int NB = PAIRED ? 2 : 1;
   constexpr int BNL = NB * BN;                  // weight rows per tile
@@ -944,7 +1004,8 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   constexpr int D = ROWS / (4 * RPI);           // DMA instructions per wave per stage
   constexpr int NS = BK / 32;                   // MFMA sub-steps per stage
   constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
-  static_assert((BK == 64 || BK == 128) && ROWS % (4 * RPI) == 0 && WGM * WGN == 4 && TI >= 1 && TJ >= 1,
+  static_assert((BK == 64 || BK == 128 || BK == 256) && ROWS % (4 * RPI) == 0 && WGM * WGN == 4 && TI >= 1 &&
+                    TJ >= 1 && NS % 2 == 0,
                 "tile shape");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
 
@@ -956,6 +1017,7 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   const int m0 = tile.m * BM, n0 = tile.n * BN;
   const int k_begin = tile.split * k_per_split;
   const int nk = k_per_split / BK;
+  const int s0 = rot > 0 ? (int)(((int64_t)tile.n * rot) % nk) : 0;
 
   // DMA instruction j covers tile rows RPI j .. RPI j + RPI - 1 (activation
   // rows first); wave w issues j = w + 4 q.  Lane l writes slot l % CH of
@@ -979,7 +1041,8 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   const char* Bb = reinterpret_cast<const char*>(B + k_begin);
   auto issue = [&](int st, int buf) {
     bf16_t* dst = lds + buf * STAGE;
-    const int kb = st * BK * 2;
+    const int k = st + s0;
+    const int kb = (k >= nk ? k - nk : k) * BK * 2;
 #pragma unroll
     for (int q = 0; q < D; ++q) {
       const bool is_a = RPI * (wave + 4 * q) < BM;  // wave-uniform
@@ -1046,16 +1109,16 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
     bf16x8 a0[TI], b0[NB][TJ], a1[TI], b1[NB][TJ];
     read_frags(base, 0, a0, b0);
     __builtin_amdgcn_sched_barrier(0);
-    read_frags(base, 1, a1, b1);
-    mfma(a0, b0);
-    interleave();
-    if constexpr (NS == 4) {
-      read_frags(base, 2, a0, b0);
-      mfma(a1, b1);
-      interleave();
-      read_frags(base, 3, a1, b1);
+#pragma unroll
+    for (int s = 0; s < NS; s += 2) {
+      read_frags(base, s + 1, a1, b1);
       mfma(a0, b0);
       interleave();
+      if (s + 2 < NS) {
+        read_frags(base, s + 2, a0, b0);
+        mfma(a1, b1);
+        interleave();
+      }
     }
     mfma(a1, b1);
     __builtin_amdgcn_sched_barrier(0);
@@ -1063,60 +1126,166 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
   // no DMA may still be writing LDS when the work-group ends
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-  // The weight fragment is the first MFMA operand, so the accumulators hold
-  // the transposed tile: lane l has row 16 i + l % 16 and the four
-  // consecutive columns 16 j + 4 (l / 16) .. + 3, stored as one 16-byte
-  // (fp32) or 8-byte (bf16) chunk where the row is aligned and the columns
-  // are inside the output.
-  const int mrow = m0 + wm0 + fr, ncol = n0 + wn0 + 4 * fg;
-  const bool to_part = partial != nullptr;
-  const bool resid = !PAIRED && !to_part && epi.mode == EPI_RESID;
-  const bool bf = !to_part && !resid && epi.out_bf16;
-  const int64_t ld = to_part ? (int64_t)NB * N : (int64_t)epi.ldo;
-  const bool aligned = to_part ? (N % 4 == 0 && (reinterpret_cast<uintptr_t>(partial) & 15) == 0)
-                               : (epi.ldo % 4 == 0 && (reinterpret_cast<uintptr_t>(epi.out) & 15) == 0);
-  float* const fbase = to_part ? partial + (int64_t)tile.split * M * ld : reinterpret_cast<float*>(epi.out);
-  bf16_t* const bbase = reinterpret_cast<bf16_t*>(epi.out);
+  stream_epilogue<NB, TI, TJ, PAIRED>(acc, m0 + wm0 + fr, n0 + wn0 + 4 * fg, M, N, tile.split, epi, partial);
+}
+
+// ------------------- bf16 MFMA GEMM, few rows, separate activation and weight rings
+// The few-row kernel above with one LDS ring for the activation rows (read
+// by every tile, resident in L2) and another for the weight rows (streamed
+// once from HBM): NA activation stages filled one step ahead and NW weight
+// stages filled NW - 1 steps ahead, so with 112 activation rows two weight
+// stages are in flight where a shared ring of the same size holds one.  The
+// copies of a step go out activation rows first, then weight rows; at step
+// t the wait leaves in flight only the weight copies issued after the
+// activation rows of step t (those of step t + NW - 2).  `rot` > 0 starts
+// tile n at K step (n rot) mod nk and wraps, which spreads the HBM rows that
+// the tiles stream at one time over more banks.  Fragment reads and the MFMA
+// tiling are those of gemm_stream_kernel; BK 128 or 256 (a copy instruction
+// then moves 4 rows of 256 bytes or 2 rows of 512 bytes).
+template <int BM, int BN, int WGM, int WGN, int NA, int NW, bool PAIRED, int BK>
+__global__ void __launch_bounds__(256)
+gemm_ring_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict__ B, int ldb, int64_t pair_off,
+                 int M, int N, int K, int k_per_split, int rot, EpiArgs epi, float* __restrict__ partial) {
+  constexpr int NB = PAIRED ? 2 : 1;
+  constexpr int BNL = NB * BN;                  // weight rows per tile
+  constexpr int CH = BK / 8;                    // 16-byte chunks per row
+  constexpr int RPI = 64 / CH;                  // rows per copy instruction (1 KB)
+  constexpr int DA = BM / (4 * RPI), DW = BNL / (4 * RPI);  // copies per wave per step
+  constexpr int NS = BK / 32;                   // MFMA sub-steps per step
+  constexpr int WM = BM / WGM, WN = BN / WGN, TI = WM / 16, TJ = WN / 16;
+  constexpr int ASZ = BM * BK, WSZ = BNL * BK;  // bf16 elements per stage
+  static_assert((BK == 128 || BK == 256) && BM % (4 * RPI) == 0 && BNL % (4 * RPI) == 0 && WGM * WGN == 4 &&
+                    TI >= 1 && TJ >= 1 && NA >= 2 && NW >= 3 && NS % 2 == 0,
+                "tile shape");
+  static_assert((NA * ASZ + NW * WSZ) * 2 <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NA * ASZ + NW * WSZ];
+
+  const TileIdx tile = tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, K / k_per_split);
+  if (!tile.valid) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+  const int m0 = tile.m * BM, n0 = tile.n * BN;
+  const int k_begin = tile.split * k_per_split;
+  const int nk = k_per_split / BK;
+  const int s0 = rot > 0 ? (int)(((int64_t)tile.n * rot) % nk) : 0;
+
+  // Copy q of a wave moves rows RPI (wave + 4 q) .. + RPI - 1 of its ring
+  // stage; lane l writes slot l % CH of row l / CH and fetches the chunk
+  // stored there.  Rows past M or N are clamped (never stored).
+  uint32_t aoff[DA], woff[DW];
 #pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const int m = mrow + 16 * i;
-    if (m >= M) continue;
+  for (int q = 0; q < DA; ++q) {
+    const int r = RPI * (wave + 4 * q) + lane / CH;
+    const int c = stream_slot<BK>(lane % CH, r);
+    aoff[q] = (uint32_t)(((int64_t)min(m0 + r, M - 1) * lda + c * 8) * 2);
+  }
 #pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      const int n = ncol + 16 * j;
-      if (n >= N) continue;
-      const bool full = aligned && n + 3 < N;
-      const int64_t off = (int64_t)m * ld + n;
-      f32x4 v = acc[0][i][j];
-      if (to_part) {
-        if (full) {
-          store4(fbase + off, v);
-          if (PAIRED) store4(fbase + off + N, acc[NB - 1][i][j]);
-        } else {
-          for (int k = 0; k < 4 && n + k < N; ++k) {
-            fbase[off + k] = v[k];
-            if (PAIRED) fbase[off + N + k] = acc[NB - 1][i][j][k];
-          }
-        }
-        continue;
-      }
-      if (PAIRED) {
+  for (int q = 0; q < DW; ++q) {
+    const int rb = RPI * (wave + 4 * q) + lane / CH;
+    const int c = stream_slot<BK>(lane % CH, rb);
+    const int blk = rb / BN;
+    woff[q] = (uint32_t)((blk * pair_off + (int64_t)min(n0 + rb - blk * BN, N - 1) * ldb + c * 8) * 2);
+  }
+  const char* Ab = reinterpret_cast<const char*>(A + k_begin);
+  const char* Bb = reinterpret_cast<const char*>(B + k_begin);
+  bf16_t* const wring = lds + NA * ASZ;
+  // byte offset of step st's K columns
+  auto kbyte = [&](int st) {
+    const int k = st + s0;
+    return (k >= nk ? k - nk : k) * BK * 2;
+  };
+  auto issue_a = [&](int st, int buf) {
+    bf16_t* dst = lds + buf * ASZ;
+    const int kb = kbyte(st);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) v[k] = silu(v[k]) * acc[NB - 1][i][j][k];
-      }
-      if (full) {
-        if (resid) v += *reinterpret_cast<const f32x4*>(fbase + off);
-        if (bf) store4(bbase + off, v);
-        else store4(fbase + off, v);
-      } else {
-        for (int k = 0; k < 4 && n + k < N; ++k) {
-          if (resid) fbase[off + k] += v[k];
-          else if (bf) bbase[off + k] = f32_to_bf16(v[k]);
-          else fbase[off + k] = v[k];
-        }
+    for (int q = 0; q < DA; ++q) dma16(Ab + kb + aoff[q], dst + (wave + 4 * q) * 512);
+  };
+  auto issue_w = [&](int st, int buf) {
+    bf16_t* dst = wring + buf * WSZ;
+    const int kb = kbyte(st);
+#pragma unroll
+    for (int q = 0; q < DW; ++q) dma16(Bb + kb + woff[q], dst + (wave + 4 * q) * 512);
+  };
+
+  const int fr = lane & 15, fg = lane >> 4;
+  int foff[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) foff[s] = fr * BK + 8 * stream_slot<BK>(4 * s + fg, fr);
+
+  f32x4 acc[NB][TI][TJ];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto read_frags = [&](const bf16_t* ab, const bf16_t* wb, int s, bf16x8(&af)[TI], bf16x8(&bfr)[NB][TJ]) {
+#pragma unroll
+    for (int i = 0; i < TI; ++i) af[i] = *reinterpret_cast<const bf16x8*>(ab + foff[s] + (wm0 + 16 * i) * BK);
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+        bfr[b][j] = *reinterpret_cast<const bf16x8*>(wb + foff[s] + (b * BN + wn0 + 16 * j) * BK);
+  };
+  auto mfma = [&](const bf16x8(&af)[TI], const bf16x8(&bfr)[NB][TJ]) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+          acc[b][i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[b][j], af[i], acc[b][i][j], 0, 0, 0);
+  };
+  constexpr int NMF = NB * TI * TJ, NRD = TI + NB * TJ;
+  auto interleave = [] {
+#pragma unroll
+    for (int k = 0; k < (NRD < NMF ? NRD : NMF); ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if constexpr (NRD > NMF) __builtin_amdgcn_sched_group_barrier(0x100, NRD - NMF, 0);
+    if constexpr (NMF > NRD) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Prologue: activation rows of step 0, weight rows of steps 0 .. NW - 2
+  // (only steps that exist: a copy past the end would be waited for before
+  // the work-group may end).
+  issue_a(0, 0);
+  for (int st = 0; st < NW - 1 && st < nk; ++st) issue_w(st, st);
+  for (int t = 0; t < nk; ++t) {
+    // Steps t of both rings landed, and every wave is done with the buffers
+    // of step t - 1 (refilled below).  Issued after the activation rows of
+    // step t: at t = 0 the weight rows of steps 1 .. NW - 2; later those of
+    // step t + NW - 2 (issued with them at step t - 1), when it exists.
+    if (t == 0) vm_barrier_ahead<DW, NW - 2>(min(NW - 2, nk - 1));
+    else vm_barrier_ahead<DW, 1>(t + NW - 2 < nk ? 1 : 0);
+    if (t + 1 < nk) issue_a(t + 1, (t + 1) % NA);
+    if (t + NW - 1 < nk) issue_w(t + NW - 1, (t + NW - 1) % NW);
+    const bf16_t* ab = lds + (t % NA) * ASZ;
+    const bf16_t* wb = wring + (t % NW) * WSZ;
+    bf16x8 a0[TI], b0[NB][TJ], a1[TI], b1[NB][TJ];
+    read_frags(ab, wb, 0, a0, b0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int s = 0; s < NS; s += 2) {
+      read_frags(ab, wb, s + 1, a1, b1);
+      mfma(a0, b0);
+      interleave();
+      if (s + 2 < NS) {
+        read_frags(ab, wb, s + 2, a0, b0);
+        mfma(a1, b1);
+        interleave();
       }
     }
+    mfma(a1, b1);
+    __builtin_amdgcn_sched_barrier(0);
   }
+  // no DMA may still be writing LDS when the work-group ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  stream_epilogue<NB, TI, TJ, PAIRED>(acc, m0 + wm0 + fr, n0 + wn0 + 4 * fg, M, N, tile.split, epi, partial);
 }
 
 // ------------------------------------------------------------ fp32 GEMM
@@ -1230,6 +1399,7 @@ constexpr int kDma3MaxRows = 512;
 constexpr int kDmaWideMinTiles = 192;
 constexpr int kDmaMinRows = 1024;
 constexpr int kBigTileMinRows = 1024;
+constexpr int kPairedRot = 7;
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : (M <= 112 ? 112 : 128)); }
 
@@ -1343,25 +1513,40 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   }
   if (plan.stream && dma_offsets_fit(g)) {
     dim3 grid = tile_grid((g.M + plan.stream - 1) / plan.stream, (g.N + plan.stream_bn - 1) / plan.stream_bn, splits);
-#define SR_STREAM(BM, BN, WGM, WGN, NST, P)                                                              \
-  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, 128>), grid, dim3(256), 0, s,          \
-                     (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, \
+#define SR_STREAM(BM, BN, WGM, WGN, NST, P, BK, ROT)                                                    \
+  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, BK>), grid, dim3(256), 0, s,           \
+                     (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, ROT, e, \
                      part)
+#define SR_RING(BM, BN, WGM, WGN, NA, NW, P, BK, ROT)                                                    \
+  hipLaunchKernelGGL((gemm_ring_kernel<BM, BN, WGM, WGN, NA, NW, P, BK>), grid, dim3(256), 0, s,          \
+                     (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, ROT, e, \
+                     part)
+    // The paired (gate and up) projections start each tile at its own K
+    // step (rotation kPairedRot); without it their tiles stream both weight
+    // blocks in lockstep and reach 4.0-4.4 TB/s, with it 5.0-5.7 (measured
+    // on the 8B shapes at 21-128 rows).
     if (plan.stream == 32) {
-      if (g.paired) SR_STREAM(32, 64, 1, 4, 3, true);
-      else SR_STREAM(32, 64, 1, 4, 5, false);
+      if (g.paired) {
+        // 2 rows of 512 bytes per copy instruction
+        if (kps % 256 == 0) SR_STREAM(32, 64, 1, 4, 2, true, 256, kPairedRot);
+        else SR_STREAM(32, 64, 1, 4, 3, true, 128, kPairedRot);
+      } else {
+        SR_STREAM(32, 64, 1, 4, 5, false, 128, 0);
+      }
     } else if (plan.stream == 64) {
-      if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true);
-      else SR_STREAM(64, 64, 2, 2, 4, false);
+      if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true, 128, kPairedRot);
+      else SR_STREAM(64, 64, 2, 2, 4, false, 128, 0);
     } else if (plan.stream == 112) {
       // 65-112 rows: seven 16-row blocks per wave, the four waves side by
-      // side over the columns (less padding than 128 rows)
-      if (g.paired) SR_STREAM(112, 64, 1, 4, 2, true);
-      else SR_STREAM(112, 64, 1, 4, 3, false);
+      // side over the columns (less padding than 128 rows); paired: two
+      // weight stages in flight beside the activation ring
+      if (g.paired) SR_RING(112, 64, 1, 4, 2, 3, true, 128, kPairedRot);
+      else SR_STREAM(112, 64, 1, 4, 3, false, 128, 0);
     } else {
-      if (g.paired) SR_STREAM(128, 64, 2, 2, 2, true);
-      else SR_STREAM(128, 64, 2, 2, 3, false);
+      if (g.paired) SR_RING(128, 64, 2, 2, 2, 3, true, 128, kPairedRot);
+      else SR_STREAM(128, 64, 2, 2, 3, false, 128, 0);
     }
+#undef SR_RING
 #undef SR_STREAM
     SR_CHECK_LAUNCH();
   } else if (plan.dma3 && dma_offsets_fit(g, 31)) {

@@ -21,8 +21,10 @@ SHAPES = [(1, 64, 64), (17, 100, 128), (33, 1000, 512), (100, 384, 4096), (129, 
           (128, 200, 1024), (64, 64, 14336), (21, 4100, 1792), (112, 130, 384),
           # a few hundred rows with enough 256 x 256 tiles for the three-deep weight ring
           (300, 49152, 256), (257, 24576, 128),
-          # the 103-row QKV projection of the 8B shape (48-column streaming tiles)
+          # the 103-row QKV projection of the 8B shape
           (103, 6144, 4096),
+          # paired few-row tiles with 512-byte rows per copy (K steps of 256), ragged N
+          (21, 4100, 2048),
           # thousands of rows, ragged in M and N, ten K steps (the 256 x 256 tile)
           (2600, 1100, 640)]
 
@@ -66,3 +68,25 @@ def test_projection(dtype, mode, M, N, K):
     scale = np.abs(ref).max()
     rtol = 1e-2 if (mode in (2, 3) and dtype == "bf16") else 1e-4
     assert np.abs(got - ref).max() <= rtol * scale, np.abs(got - ref).max()
+
+
+@pytest.mark.parametrize("M", [8, 41, 103, 120])
+def test_projection_paired_8b(M):
+    """The 8B gate/up projection (N 14336, K 4096) at the row counts of the
+    decode rounds: every few-row tile kind with its rotated K order."""
+    torch, sr = need_gpu()
+    N, K = 14336, 4096
+    say(f"paired projection bf16 M={M} N={N} K={K}")
+    rng = np.random.default_rng(M)
+    x = bf16_round(rng.normal(0, 1, size=(M, K)).astype(np.float32))
+    w = bf16_round(rng.normal(0, 0.02, size=(2, N, K)).astype(np.float32))
+    xt = torch.from_numpy((x.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).cuda()
+    wt = torch.from_numpy((w.view(np.uint32) >> 16).astype(np.uint16).view(np.int16)).cuda()
+    out = torch.zeros((M, N), dtype=torch.int16, device="cuda")
+    sr.projection(xt, wt, 2, out)
+    torch.cuda.synchronize()
+    got = (out.cpu().numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    x64, w64 = x.astype(np.float64), w.astype(np.float64)
+    g, u = x64 @ w64[0].T, x64 @ w64[1].T
+    ref = g / (1 + np.exp(-g)) * u
+    assert np.abs(got - ref).max() <= 1e-2 * np.abs(ref).max(), np.abs(got - ref).max()
