@@ -1399,7 +1399,7 @@ constexpr int kDma3MaxRows = 512;
 constexpr int kDmaWideMinTiles = 192;
 constexpr int kDmaMinRows = 1024;
 constexpr int kBigTileMinRows = 1024;
-constexpr int kPairedRot = 7;
+constexpr int kTileRot = 7;
 
 static int stream_tile_rows(int M) { return M <= 32 ? 32 : (M <= 64 ? 64 : (M <= 112 ? 112 : 128)); }
 
@@ -1522,28 +1522,28 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, ROT, e, \
                      part)
     // The paired (gate and up) projections start each tile at its own K
-    // step (rotation kPairedRot); without it their tiles stream both weight
+    // step (rotation kTileRot); without it their tiles stream both weight
     // blocks in lockstep and reach 4.0-4.4 TB/s, with it 5.0-5.7 (measured
     // on the 8B shapes at 21-128 rows).
     if (plan.stream == 32) {
       if (g.paired) {
         // 2 rows of 512 bytes per copy instruction
-        if (kps % 256 == 0) SR_STREAM(32, 64, 1, 4, 2, true, 256, kPairedRot);
-        else SR_STREAM(32, 64, 1, 4, 3, true, 128, kPairedRot);
+        if (kps % 256 == 0) SR_STREAM(32, 64, 1, 4, 2, true, 256, kTileRot);
+        else SR_STREAM(32, 64, 1, 4, 3, true, 128, kTileRot);
       } else {
         SR_STREAM(32, 64, 1, 4, 5, false, 128, 0);
       }
     } else if (plan.stream == 64) {
-      if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true, 128, kPairedRot);
+      if (g.paired) SR_STREAM(64, 64, 2, 2, 3, true, 128, kTileRot);
       else SR_STREAM(64, 64, 2, 2, 4, false, 128, 0);
     } else if (plan.stream == 112) {
       // 65-112 rows: seven 16-row blocks per wave, the four waves side by
       // side over the columns (less padding than 128 rows); paired: two
       // weight stages in flight beside the activation ring
-      if (g.paired) SR_RING(112, 64, 1, 4, 2, 3, true, 128, kPairedRot);
+      if (g.paired) SR_RING(112, 64, 1, 4, 2, 3, true, 128, kTileRot);
       else SR_STREAM(112, 64, 1, 4, 3, false, 128, 0);
     } else {
-      if (g.paired) SR_RING(128, 64, 2, 2, 2, 3, true, 128, kPairedRot);
+      if (g.paired) SR_RING(128, 64, 2, 2, 2, 3, true, 128, kTileRot);
       else SR_STREAM(128, 64, 2, 2, 3, false, 128, 0);
     }
 #undef SR_RING

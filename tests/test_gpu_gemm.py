@@ -23,6 +23,8 @@ SHAPES = [(1, 64, 64), (17, 100, 128), (33, 1000, 512), (100, 384, 4096), (129, 
           (300, 49152, 256), (257, 24576, 128),
           # the 103-row QKV projection of the 8B shape
           (103, 6144, 4096),
+          # 65-112 rows, long K, ragged N
+          (70, 2000, 8192), (103, 4096, 14336),
           # paired few-row tiles with 512-byte rows per copy (K steps of 256), ragged N
           (21, 4100, 2048),
           # thousands of rows, ragged in M and N, ten K steps (the 256 x 256 tile)
