@@ -31,6 +31,11 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float exp2_or_zero(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
 
+// Work-group barrier after this wave's LDS reads and writes complete; vector
+// memory loads issued before it stay in flight (__syncthreads would wait for
+// them too).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // DPP move within rows of 16 lanes (ctrl: quad_perm 0x00-0xff, row_mirror
 // 0x140, row_half_mirror 0x141).
 template <int CTRL>
@@ -1253,9 +1258,11 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 
 // --------------------------------------------------------- prefill (MFMA)
 // bf16 flash attention with v_mfma_f32_16x16x32_bf16, head_dim 64 or 128.
-// Work-group = one row,
-// one KV head, 16 queries; wave w computes query head (kvh * G + w) for those
-// queries, so the G waves share every K/V tile staged in LDS (32 keys).
+// Work-group = one row, one KV head, 16 queries; wave w computes query head
+// (kvh * G + w) for those queries, so the G waves share every K/V tile
+// staged in LDS (32 keys).  (Two or four 16-query blocks per wave reuse a
+// tile more but hold too many registers for more than one or two
+// work-groups per SIMD, and measured slower.)
 //   S^T = K Q^T   (keys x queries): lane l holds keys 4(l/16)+i (+16 for the
 //                 second key tile) of query l%16, so the online-softmax state
 //                 of a query lives in one lane group (max/sum over l/16).
@@ -1264,6 +1271,8 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 //                 S^T values (keys 4g..4g+3 of tile 0, then of tile 1); the A
 //                 operand comes from the V tile, staged row by row like K, by
 //                 two LDS transpose reads.
+// The next 32-key tile is fetched into registers while the current one is
+// computed.
 constexpr int PF_KT = 32;            // keys per tile
 
 // PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
@@ -1272,9 +1281,6 @@ constexpr int PF_KT = 32;            // keys per tile
 // and left part_splits partial slots per (row, query head) in `part`
 // (unnormalised output, running max, sum); the work-group folds them into
 // its own result by log-sum-exp and writes the attention output.
-// The prefix form fetches the next 32-key tile into registers while the
-// current one is computed (the prefill form, with many work-groups per CU,
-// fetches each tile just before staging it).
 template <int HD, int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
@@ -1295,17 +1301,26 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   const int qh = h * G + wave;
   const int t = qb * 16 + fr;              // this lane's query (as B column / C column)
   const bool qvalid = t < lr;
-  // Q^T fragments: lane holds Q[t][32 s + 8 fg .. +8] for k-step s (scaled, bf16)
+  // Q^T fragments: lane holds Q[t][32 s + 8 fg .. +8] for k-step s (scaled,
+  // bf16); loaded from a clamped row, unconditionally, so all go out at once
   bf16x8 qf[KS];
   {
-    const float* qr = q + (((int64_t)row * lr + (qvalid ? t : 0)) * hq + qh) * HD;
+    const float sc = qvalid ? qscale : 0.f;
+    const float4* qr = reinterpret_cast<const float4*>(q + (((int64_t)row * lr + min(t, lr - 1)) * hq + qh) * HD);
+    float4 qv[2 * KS];
 #pragma unroll
-    for (int st = 0; st < KS; ++st)
+    for (int st = 0; st < KS; ++st) {
+      qv[2 * st] = qr[8 * st + 2 * fg];
+      qv[2 * st + 1] = qr[8 * st + 2 * fg + 1];
+    }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float v = qvalid ? qr[32 * st + 8 * fg + e] * qscale : 0.f;
-        qf[st][e] = (__bf16)v;
-      }
+    for (int st = 0; st < KS; ++st) {
+      const float4 a = qv[2 * st], b = qv[2 * st + 1];
+      qf[st][0] = (__bf16)(a.x * sc); qf[st][1] = (__bf16)(a.y * sc);
+      qf[st][2] = (__bf16)(a.z * sc); qf[st][3] = (__bf16)(a.w * sc);
+      qf[st][4] = (__bf16)(b.x * sc); qf[st][5] = (__bf16)(b.y * sc);
+      qf[st][6] = (__bf16)(b.z * sc); qf[st][7] = (__bf16)(b.w * sc);
+    }
   }
   f32x4 o[DT];
 #pragma unroll
@@ -1334,21 +1349,12 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       }
     }
   };
-  if constexpr (PREFIX_ONLY) fetch(0);
-  for (int kb = 0; kb < nkeys; kb += PF_KT) {
-    // stage K [key][dim] and V^T [dim][key] (prefix form: then fetch the next tile)
-    if constexpr (!PREFIX_ONLY) fetch(kb);
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = threadIdx.x + NT * i;
-      if (c >= PF_KT * CPK) break;
-      const int j = c / CPK, cc = c % CPK;
-      *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
-      *reinterpret_cast<uint4*>(&Vs[j * PF_VROW + cc * 8]) = vreg[i];
-    }
-    __syncthreads();
-    if constexpr (PREFIX_ONLY)
-      if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
+  // Lane i of a group names dims dt 16 + 4 (i & 3) .. + 3 of key
+  // 4 fg + (i >> 2) (and 16 keys on), so it receives dim dt 16 + i of keys
+  // 4 fg .. + 3 (and 16 + 4 fg .. + 3): the A operand rows of O^T += V^T P^T
+  const bf16_t* vb = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
+  // the staged tile of keys kb .. kb + 31
+  auto compute = [&](int kb) {
     // S^T for key tiles 0 (keys kb..kb+15) and 1 (kb+16..kb+31)
     f32x4 st[2];
 #pragma unroll
@@ -1389,11 +1395,6 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     ls += __shfl_xor(ls, 32, 64);
     l = l * corr + ls;
     m = mn;
-    // O^T += V^T P^T over the 32 keys in the permuted order.  Lane i of a
-    // group names dims dt 16 + 4 (i & 3) .. + 3 of key 4 fg + (i >> 2) (and
-    // 16 keys on), so it receives dim dt 16 + i of keys 4 fg .. + 3 (and
-    // 16 + 4 fg .. + 3): the A operand rows
-    const bf16_t* vb = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       o[dt] *= corr;
@@ -1401,7 +1402,23 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       const i16x4 hi = lds_read_tr16(vb + 16 * PF_VROW + dt * 16);
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tr16_pair(lo, hi), pf, o[dt], 0, 0, 0);
     }
-    __syncthreads();
+  };
+  fetch(0);
+  for (int kb = 0; kb < nkeys; kb += PF_KT) {
+    // stage K [key][dim] and V [key][dim]
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = threadIdx.x + NT * i;
+      if (PF_KT * CPK % NT == 0 || c < PF_KT * CPK) {
+        const int j = c / CPK, cc = c % CPK;
+        *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
+        *reinterpret_cast<uint4*>(&Vs[j * PF_VROW + cc * 8]) = vreg[i];
+      }
+    }
+    lds_barrier();
+    if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
+    compute(kb);
+    lds_barrier();
   }
   if (qvalid) {
     if (PREFIX_ONLY) {

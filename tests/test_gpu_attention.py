@@ -94,10 +94,13 @@ PREFILL_CASES = [
     # dtype, hd, hq, hkv, rows, P, t0, lr, cap
     ("bf16", 128, 32, 8, 3, 40, 37, 29, 70),      # matrix-core kernel, ragged tiles
     ("bf16", 128, 32, 8, 2, 256, 128, 100, 636),  # 8B shapes: second scoring round
+    ("bf16", 128, 32, 8, 2, 256, 0, 128, 128),    # 8B shapes: first scoring round (64-query blocks)
+    ("bf16", 128, 32, 8, 2, 7, 45, 130, 200),     # 64-query blocks, ragged last block
+    ("bf16", 64, 32, 8, 2, 30, 3, 150, 160),      # head_dim 64, 64-query blocks
     ("bf16", 128, 8, 8, 2, 0, 16, 33, 49),
     ("bf16", 128, 16, 2, 2, 17, 0, 50, 64),
     ("bf16", 128, 32, 8, 1, 5, 0, 1, 1),
-    ("bf16", 64, 8, 2, 3, 33, 20, 17, 40),         # vector kernel
+    ("bf16", 64, 8, 2, 3, 33, 20, 17, 40),
     ("f32", 32, 4, 4, 2, 5, 9, 11, 20),
     ("f32", 64, 8, 2, 1, 0, 0, 1, 1),
     ("f32", 32, 8, 1, 2, 3, 64, 40, 110),
