@@ -890,7 +890,7 @@ constexpr int kWaveTarget = 2048;
 template <int HD, int G, bool PREFIX_ONLY>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
-                                         const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq,
+                                         const bf16_t* __restrict__ vown, int rows, int lr, int cap, int t0, int hq,
                                          int hkv, bf16_t* __restrict__ out, float qscale,
                                          float* __restrict__ part, int part_splits);
 
@@ -1001,7 +1001,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   // result, so no merge pass is needed.
   auto prefix_pass = [&](int tsplits) {
     hipLaunchKernelGGL((prefill_attn_mfma_kernel<128, G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
-                       a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, a.rows, 0, 0, a.hq,
+                       a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, 1, a.rows, 0, 0, a.hq,
                        a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
     SR_CHECK_LAUNCH();
   };
@@ -1285,7 +1285,7 @@ template <int HD, int G, bool PREFIX_ONLY>
 __global__ void __launch_bounds__(64 * G)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
-                         const bf16_t* __restrict__ vown, int lr, int cap, int t0, int hq, int hkv,
+                         const bf16_t* __restrict__ vown, int rows, int lr, int cap, int t0, int hq, int hkv,
                          bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
   constexpr int NT = 64 * G;
   constexpr int KS = HD / 32, DT = HD / 16, CPK = HD / 8;
@@ -1295,7 +1295,24 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   static_assert(HD == 64 || HD == 128, "head_dim");
   __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[PF_KT * PF_VROW];
-  const int qb = blockIdx.x, h = blockIdx.y, row = PREFIX_ONLY ? 0 : blockIdx.z;
+  // The prefill form runs a 1-D grid of 8 C work-groups, dealt round-robin
+  // to the 8 XCDs: XCD x takes the consecutive logical blocks
+  // [x C, (x + 1) C), ordered query block fastest, so the query blocks that
+  // read the same row's keys share one L2.
+  int qb, h, row;
+  if constexpr (PREFIX_ONLY) {
+    qb = blockIdx.x;
+    h = blockIdx.y;
+    row = 0;
+  } else {
+    const int nqb = (lr + 15) / 16, total = nqb * hkv * rows;
+    const int per_xcd = (total + 7) / 8;
+    const int pid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (pid >= total) return;
+    qb = pid % nqb;
+    h = (pid / nqb) % hkv;
+    row = pid / (nqb * hkv);
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fg = lane >> 4;
   const int qh = h * G + wave;
@@ -1492,10 +1509,12 @@ static void prefill_by_hd(const PrefillAttnArgs& a, hipStream_t s) {
 template <int HD, int G>
 static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
-  dim3 grid((a.lr + 15) / 16, a.hkv, a.rows);
+  const int64_t total = (int64_t)((a.lr + 15) / 16) * a.hkv * a.rows;
+  SR_REQUIRE(total <= (int64_t)INT32_MAX - 8, SR_ERR_UNSUPPORTED, "prefill attention grid too large");
+  dim3 grid((unsigned)(8 * ((total + 7) / 8)));
   hipLaunchKernelGGL((prefill_attn_mfma_kernel<HD, G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
-                     (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.lr, a.cap, a.t0,
-                     a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
+                     (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.rows, a.lr, a.cap,
+                     a.t0, a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();
 }
 
