@@ -592,8 +592,9 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
       for (int j = 0; j < 4; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
   };
-  // instruction interleavings: (MFMA, fragment read) x 16; (MFMA, read) x 8
-  // then 8 MFMAs; (2 MFMAs, DMA) x 8; (MFMA, read, MFMA, DMA) x 8
+  // instruction interleavings before the step barrier: (MFMA, fragment
+  // read) x 16; (MFMA, read) x 8 then 8 MFMAs (after it the order is written
+  // out: the scheduler bunched the copies behind one MFMA)
   auto reads16 = [] {
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -609,24 +610,6 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  auto dma8 = [] {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  auto reads8_dma8 = [] {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-    }
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -667,14 +650,36 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict_
     if constexpr (BRING == 3) SR_VM_BARRIER(8);
     else SR_VM_BARRIER(0);
     __builtin_amdgcn_sched_barrier(0);
-    issue_half(nx, buf, 0);
-    // (after the last step this reads a stale buffer that is never used)
-    read_frags(buf ^ 1, bbn, 0, ya, yb);
-    mfma(za, zb);
-    reads8_dma8();
-    issue_half(nxb, bb, 1);
-    mfma(xa, xb);
-    dma8();
+    // Quarter 2 with the A rows of step t + 2 and the next step's quarter-0
+    // fragments (after the last step a stale buffer that is never used):
+    // one copy and one read per pair of MFMAs, in this order.
+    {
+      bf16_t* dst = a_base(buf);
+      const bf16_t* sa = a_base(buf ^ 1) + foff[0];
+      const bf16_t* sb = b_base(bbn) + foff[0];
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const int i = p >> 1, j = (p & 1) * 2;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zb[j], za[i], acc[i][j], 0, 0, 0);
+        acc[i][j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(zb[j + 1], za[i], acc[i][j + 1], 0, 0, 0);
+        dma16(ra, aoff[p], nx * BK * 2, dst + (wave + 4 * p) * 512);
+        if (p < 4) ya[p] = *reinterpret_cast<const bf16x8*>(sa + (wm0 + 32 * p) * BK);
+        else yb[p - 4] = *reinterpret_cast<const bf16x8*>(sb + (wn0 + 32 * (p - 4)) * BK);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // Quarter 3 with the B rows of step t + BRING, one copy per MFMA pair.
+    {
+      bf16_t* dst = b_base(bb);
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const int i = p >> 1, j = (p & 1) * 2;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xb[j], xa[i], acc[i][j], 0, 0, 0);
+        acc[i][j + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xb[j + 1], xa[i], acc[i][j + 1], 0, 0, 0);
+        dma16(rb, boff[p], nxb * BK * 2, dst + (wave + 4 * p) * 512);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
   };
   for (int t = 0; t < nk; t += 3) {
     // B ring slots: t % 3 with three (t is a multiple of 3 here), t % 2 with two
@@ -778,36 +783,6 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-  auto mfma = [&](const bf16x8(&af)[4], const bf16x8(&bfr)[2]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
-  };
-  // quarters 0-2: (MFMA, read, MFMA, DMA) x 4, then the last two reads
-  auto reads_dmas = [] {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-  // quarter 3 (and quarters 0-2 of the last two steps): (MFMA, read) x 6, then 2 MFMAs
-  auto reads = [] {
-#pragma unroll
-    for (int q = 0; q < 6; ++q) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
   // Every step issues the DMAs of the step after next (clamped to the last
   // step past the end: data never read), so every wait is the same.
 #pragma unroll
@@ -821,49 +796,41 @@ gemm_dma3_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restrict
   // One step; `live`: the step after next exists and is fetched (the last
   // two steps fetch nothing and wait for every copy, so no copy is in flight
   // at the end).
+  // One quarter step: the MFMAs of (af, bfr), the fragments of quarter rq
+  // of buffer rbuf into (na, nb2) and, with FETCH, copies d0 .. d0 + 3 of
+  // step nx into buffer wb, in the order (MFMA, read, MFMA, copy) x 4 and
+  // the two B reads (written out: the scheduler bunched the copies).
+  auto quarter = [&](auto fetch, const bf16x8(&af)[4], const bf16x8(&bfr)[2], int rbuf, int rq, bf16x8(&na)[4],
+                     bf16x8(&nb2)[2], int nx, int wb, int d0) {
+    constexpr bool FETCH = decltype(fetch)::value;
+    const bf16_t* sa = lds + rbuf * STAGE + foff[rq];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[0], af[i], acc[i][0], 0, 0, 0);
+      na[i] = *reinterpret_cast<const bf16x8*>(sa + (wm0 + 32 * i) * BK);
+      acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfr[1], af[i], acc[i][1], 0, 0, 0);
+      if constexpr (FETCH) dma(nx, wb, d0 + i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) nb2[j] = *reinterpret_cast<const bf16x8*>(sa + (BM + wn0 + 32 * j) * BK);
+    __builtin_amdgcn_sched_barrier(0);
+  };
   auto step = [&](auto live, int t) {
     constexpr bool FETCH = decltype(live)::value;
     const int buf = t % 3, nb = (t + 1) % 3, wb = (t + 2) % 3;
     const int nx = t + 2;
-    read_frags(buf, 1, a1, b1);
-    if constexpr (FETCH) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dma(nx, wb, i);
-      mfma(a0, b0);
-      reads_dmas();
-    } else {
-      mfma(a0, b0);
-      reads();
-    }
-    read_frags(buf, 2, a0, b0);
-    if constexpr (FETCH) {
-#pragma unroll
-      for (int i = 4; i < 8; ++i) dma(nx, wb, i);
-      mfma(a1, b1);
-      reads_dmas();
-    } else {
-      mfma(a1, b1);
-      reads();
-    }
-    read_frags(buf, 3, a1, b1);
-    if constexpr (FETCH) {
-#pragma unroll
-      for (int i = 8; i < 12; ++i) dma(nx, wb, i);
-      mfma(a0, b0);
-      reads_dmas();
-      // step t + 1 landed (all but this wave's 12 newest DMAs) in every
-      // wave, and every wave has read all it needs of buffer `buf`
-      SR_VMB3(12);
-    } else {
-      mfma(a0, b0);
-      reads();
-      SR_VMB3(0);
-    }
+    quarter(live, a0, b0, buf, 1, a1, b1, nx, wb, 0);
+    quarter(live, a1, b1, buf, 2, a0, b0, nx, wb, 4);
+    quarter(live, a0, b0, buf, 3, a1, b1, nx, wb, 8);
+    // step t + 1 landed (all but this wave's 12 newest DMAs; none in the
+    // last two steps) in every wave, and every wave has read all it needs
+    // of buffer `buf`
+    if constexpr (FETCH) SR_VMB3(12);
+    else SR_VMB3(0);
     __builtin_amdgcn_sched_barrier(0);
     // (after the last step this reads a stale buffer that is never used)
-    read_frags(nb, 0, a0, b0);
-    mfma(a1, b1);
-    reads();
+    quarter(std::false_type{}, a1, b1, nb, 0, a0, b0, 0, 0, 0);
   };
   int t = 0;
   for (; t < nk - 2; ++t) step(std::true_type{}, t);
