@@ -964,7 +964,7 @@ static void launch_group(const DecodeAttnArgs& a, float qscale, hipStream_t s) {
   const int wpr = group_wpr(G, a.rows, a.hkv);
   dim3 grid(1, a.hkv, (a.rows + R - 1) / R);
 #define SR_GROUP(W)                                                                                               \
-  hipLaunchKernelGGL((decode_group_kernel<HD, G, W>), grid, dim3(64 * R * W), 0, s, a.q, (const bf16_t*)a.kpre,  \
+  SR_LAUNCH((decode_group_kernel<HD, G, W>), grid, dim3(64 * R * W), 0, s, a.q, (const bf16_t*)a.kpre,  \
                      (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail, a.cap, a.lt, a.hq, a.hkv,   \
                      a.rows, 1, a.part, (bf16_t*)a.out, qscale, a.qpart, a.qsplits, a.qkv_dim, a.rope)
   if constexpr (G != 2) {
@@ -981,7 +981,7 @@ template <int HD, int G>
 static void launch_wave(const DecodeAttnArgs& a, int key0, const WavePlan& w, bool direct, float qscale,
                         hipStream_t s) {
 #define SR_WAVE(NW)                                                                                              \
-  hipLaunchKernelGGL((decode_wave_kernel<HD, G, NW>), dim3(w.splits, a.hkv, a.rows), dim3(64 * NW), 0, s, a.q,  \
+  SR_LAUNCH((decode_wave_kernel<HD, G, NW>), dim3(w.splits, a.hkv, a.rows), dim3(64 * NW), 0, s, a.q,  \
                      (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, (bf16_t*)a.ktail, (bf16_t*)a.vtail,       \
                      a.cap, a.lt, a.hq, a.hkv, w.kpw, key0, w.splits, a.part, direct ? (bf16_t*)a.out : nullptr, \
                      qscale, a.qpart, a.qsplits, a.qkv_dim, a.rope, a.qout)
@@ -1000,7 +1000,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   // runs last: the tails leave partial slots and it folds them into its own
   // result, so no merge pass is needed.
   auto prefix_pass = [&](int tsplits) {
-    hipLaunchKernelGGL((prefill_attn_mfma_kernel<128, G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
+    SR_LAUNCH((prefill_attn_mfma_kernel<128, G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
                        a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, 1, a.rows, 0, 0, a.hq,
                        a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
     SR_CHECK_LAUNCH();
@@ -1034,7 +1034,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
         if (pre) {
           prefix_pass(w.splits);
         } else if (!direct) {
-          hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, w.splits,
+          SR_LAUNCH((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part, w.splits,
                              (T*)a.out);
           SR_CHECK_LAUNCH();
         }
@@ -1052,7 +1052,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
     SR_REQUIRE((size_t)a.rows * a.hq * std::max(tsplits, 1) * (HD + 2) <= a.part_cap, 5,
                "attention partial buffer too small");
     if (tsplits > 0) {
-      hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
+      SR_LAUNCH((decode_attn_kernel<T, HD, G>), dim3(tsplits, a.hkv, a.rows), dim3(256), 0, s, a.q,
                          (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail, (const T*)a.vtail, a.cap,
                          a.lt, a.hq, a.hkv, tkps, tsplits, a.part, (T*)nullptr, qscale, a.P, 0);
       SR_CHECK_LAUNCH();
@@ -1066,13 +1066,13 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   if (splits > 1)
     SR_REQUIRE((size_t)a.rows * a.hq * splits * (HD + 2) <= a.part_cap, 5,
                "attention partial buffer too small");
-  hipLaunchKernelGGL((decode_attn_kernel<T, HD, G>), dim3(splits, a.hkv, a.rows), dim3(256), 0, s,
+  SR_LAUNCH((decode_attn_kernel<T, HD, G>), dim3(splits, a.hkv, a.rows), dim3(256), 0, s,
                      a.q, (const T*)a.kpre, (const T*)a.vpre, a.P, (const T*)a.ktail,
                      (const T*)a.vtail, a.cap, a.lt, a.hq, a.hkv, kps, splits, a.part,
                      splits == 1 ? (T*)a.out : (T*)nullptr, qscale, 0, 0);
   SR_CHECK_LAUNCH();
   if (splits > 1) {
-    hipLaunchKernelGGL((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part,
+    SR_LAUNCH((decode_merge_kernel<T, HD>), dim3(a.rows * a.hq), dim3(HD), 0, s, a.part,
                        splits, (T*)a.out);
     SR_CHECK_LAUNCH();
   }
@@ -1479,7 +1479,7 @@ static void launch_prefill(const PrefillAttnArgs& a, hipStream_t s) {
   constexpr int QB = 64 / G;
   const float qscale = kLog2e / sqrtf((float)HD);
   dim3 grid((a.lr + QB - 1) / QB, a.hkv, a.rows);
-  hipLaunchKernelGGL((prefill_attn_kernel<T, HD, G>), grid, dim3(256), 0, s, a.q, (const T*)a.kpre,
+  SR_LAUNCH((prefill_attn_kernel<T, HD, G>), grid, dim3(256), 0, s, a.q, (const T*)a.kpre,
                      (const T*)a.vpre, a.P, (const T*)a.kown, (const T*)a.vown, a.lr, a.cap, a.t0, a.hq,
                      a.hkv, (T*)a.out, qscale);
   SR_CHECK_LAUNCH();
@@ -1512,7 +1512,7 @@ static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
   const int64_t total = (int64_t)((a.lr + 15) / 16) * a.hkv * a.rows;
   SR_REQUIRE(total <= (int64_t)INT32_MAX - 8, SR_ERR_UNSUPPORTED, "prefill attention grid too large");
   dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-  hipLaunchKernelGGL((prefill_attn_mfma_kernel<HD, G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
+  SR_LAUNCH((prefill_attn_mfma_kernel<HD, G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
                      (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.rows, a.lr, a.cap,
                      a.t0, a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();

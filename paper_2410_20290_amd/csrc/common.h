@@ -1,6 +1,7 @@
 // Shared device/host helpers of the Speculative Rejection library (gfx950).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -114,6 +115,30 @@ void set_error(const std::string& msg);
   } while (0)
 
 #define SR_CHECK_LAUNCH() SR_HIP(hipGetLastError())
+
+// Optional timing of kernel launches by their own dispatch packets.  While
+// sr::launch_timing points at a pair of events, every launch through
+// SR_LAUNCH stamps the end of its kernel into `stop` (the last launch wins)
+// and the first one also the start of its kernel into `start`; no marker
+// packets go between the kernels.  Without it SR_LAUNCH is a plain launch.
+namespace sr {
+struct LaunchTiming {
+  hipEvent_t start, stop;
+  bool started;
+};
+extern thread_local LaunchTiming* launch_timing;
+}  // namespace sr
+#define SR_LAUNCH(kernel, grid, block, shmem, stream, ...)                                                  \
+  do {                                                                                                      \
+    sr::LaunchTiming* lt_ = sr::launch_timing;                                                            \
+    if (lt_) {                                                                                              \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, lt_->started ? nullptr : lt_->start, lt_->stop, \
+                            0, __VA_ARGS__);                                                              \
+      lt_->started = true;                                                                                  \
+    } else {                                                                                                \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                                  \
+    }                                                                                                       \
+  } while (0)
 
 #define SR_REQUIRE(cond, code, text)                \
   do {                                              \

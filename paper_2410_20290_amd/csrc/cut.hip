@@ -83,7 +83,7 @@ select_kernel(const float* __restrict__ score, const int32_t* __restrict__ cand,
 void select_topk(const float* score, const int32_t* cand, int b, int keep, int32_t* accept,
                  hipStream_t s) {
   SR_REQUIRE(b >= 1 && b <= kCutMax, 3, "cut supports 1..4096 rows");
-  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kCutThreads), 0, s, score, cand, b, keep, accept);
+  SR_LAUNCH(select_kernel, dim3(1), dim3(kCutThreads), 0, s, score, cand, b, keep, accept);
   SR_CHECK_LAUNCH();
 }
 
@@ -134,7 +134,7 @@ __global__ void __launch_bounds__(kCutThreads) cut_kernel(CutArgs a) {
 
 void cut(const CutArgs& a, hipStream_t s) {
   SR_REQUIRE(a.b >= 1 && a.b <= kCutMax, 3, "cut supports 1..4096 rows");
-  hipLaunchKernelGGL(cut_kernel, dim3(1), dim3(kCutThreads), 0, s, a);
+  SR_LAUNCH(cut_kernel, dim3(1), dim3(kCutThreads), 0, s, a);
   SR_CHECK_LAUNCH();
 }
 
@@ -181,7 +181,7 @@ void compact(const CompactArgs& a, hipStream_t s) {
   const int32_t* count = a.count;
   if (a.keep_flag) {
     SR_REQUIRE(a.b >= 1 && a.b <= kCutMax, 3, "compaction supports 1..4096 rows");
-    hipLaunchKernelGGL(pack_flags_kernel, dim3(1), dim3(kCutThreads), 0, s, a.keep_flag, a.b,
+    SR_LAUNCH(pack_flags_kernel, dim3(1), dim3(kCutThreads), 0, s, a.keep_flag, a.b,
                        a.scratch_src_row, a.new_count);
     SR_CHECK_LAUNCH();
     src_row = a.scratch_src_row;
@@ -191,7 +191,7 @@ void compact(const CompactArgs& a, hipStream_t s) {
   const int row_bytes = a.hd * a.elem_bytes;
   SR_REQUIRE(row_bytes % 16 == 0, 3, "KV row must be a multiple of 16 bytes");
   dim3 grid(a.max_rows, a.hkv, 2 * a.n_layers);
-  hipLaunchKernelGGL(compact_kernel, grid, dim3(256), 0, s, (const uint8_t*)a.src,
+  SR_LAUNCH(compact_kernel, grid, dim3(256), 0, s, (const uint8_t*)a.src,
                      a.src_block * a.elem_bytes, (uint8_t*)a.dst, a.dst_block * a.elem_bytes, src_row,
                      count, a.hkv, row_bytes, a.cap_src, a.cap_dst, a.len);
   SR_CHECK_LAUNCH();
@@ -229,7 +229,7 @@ argmax_kernel(const float* __restrict__ score, const int32_t* __restrict__ cand,
 
 void argmax_best(const float* score, const int32_t* cand, const int32_t* n_dev, int n_max,
                  int32_t* best, hipStream_t s) {
-  hipLaunchKernelGGL(argmax_kernel, dim3(1), dim3(kCutThreads), 0, s, score, cand, n_dev, n_max, best);
+  SR_LAUNCH(argmax_kernel, dim3(1), dim3(kCutThreads), 0, s, score, cand, n_dev, n_max, best);
   SR_CHECK_LAUNCH();
 }
 

@@ -20,9 +20,9 @@ __global__ void embed_kernel(const T* __restrict__ E, int d, const int32_t* __re
 void embed(int dtype, const void* E, int d, const int32_t* tok, int rows, float* h, hipStream_t s) {
   if (rows <= 0) return;
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, (const bf16_t*)E, d, tok, h);
+    SR_LAUNCH(embed_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, (const bf16_t*)E, d, tok, h);
   else
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)E, d, tok, h);
+    SR_LAUNCH(embed_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)E, d, tok, h);
   SR_CHECK_LAUNCH();
 }
 
@@ -103,7 +103,7 @@ void rmsnorm(int dtype, const float* x, int ldx, const void* g, int d, float eps
                    (reinterpret_cast<uintptr_t>(g) & 15) == 0;
   const int kv = (d / 4 + 255) / 256;
 #define SR_NORM(T, KV)                                                                                     \
-  hipLaunchKernelGGL((rmsnorm_vec_kernel<T, KV>), dim3(rows), dim3(256), 0, s, x, ldx, (const T*)g, d, eps, \
+  SR_LAUNCH((rmsnorm_vec_kernel<T, KV>), dim3(rows), dim3(256), 0, s, x, ldx, (const T*)g, d, eps, \
                      (T*)out, ldo)
   if (vec && dtype == SR_BF16) {
     if (kv <= 1) SR_NORM(bf16_t, 1);
@@ -114,10 +114,10 @@ void rmsnorm(int dtype, const float* x, int ldx, const void* g, int d, float eps
     else if (kv <= 2) SR_NORM(float, 2);
     else SR_NORM(float, 4);
   } else if (dtype == SR_BF16) {
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, ldx, (const bf16_t*)g, d,
+    SR_LAUNCH(rmsnorm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, x, ldx, (const bf16_t*)g, d,
                        eps, (bf16_t*)out, ldo);
   } else {
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, x, ldx, (const float*)g, d,
+    SR_LAUNCH(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, x, ldx, (const float*)g, d,
                        eps, (float*)out, ldo);
   }
 #undef SR_NORM
@@ -139,7 +139,7 @@ __global__ void rope_table_kernel(float2* tab, int npos, int hd, double theta) {
 void rope_table(float2* tab, int npos, int hd, double theta, hipStream_t s) {
   int64_t total = (int64_t)npos * (hd / 2);
   int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
-  hipLaunchKernelGGL(rope_table_kernel, dim3(blocks), dim3(256), 0, s, tab, npos, hd, theta);
+  SR_LAUNCH(rope_table_kernel, dim3(blocks), dim3(256), 0, s, tab, npos, hd, theta);
   SR_CHECK_LAUNCH();
 }
 
@@ -186,10 +186,10 @@ void rope_scatter(int dtype, const float* qkv, int rows, int lr, int hq, int hkv
   if (rows <= 0 || lr <= 0) return;
   dim3 grid(rows * lr);
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(rope_scatter_kernel<bf16_t>, grid, dim3(256), 0, s, qkv, lr, hq, hkv, hd, tab,
+    SR_LAUNCH(rope_scatter_kernel<bf16_t>, grid, dim3(256), 0, s, qkv, lr, hq, hkv, hd, tab,
                        pos0, qout, (bf16_t*)kdst, (bf16_t*)vdst, cap, t0);
   else
-    hipLaunchKernelGGL(rope_scatter_kernel<float>, grid, dim3(256), 0, s, qkv, lr, hq, hkv, hd, tab,
+    SR_LAUNCH(rope_scatter_kernel<float>, grid, dim3(256), 0, s, qkv, lr, hq, hkv, hd, tab,
                        pos0, qout, (float*)kdst, (float*)vdst, cap, t0);
   SR_CHECK_LAUNCH();
 }
@@ -219,10 +219,10 @@ void embed_norm(int dtype, const void* E, int d, const int32_t* tok, int rows, c
                 float* h, void* xn, hipStream_t s) {
   if (rows <= 0) return;
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, (const bf16_t*)E, d, tok,
+    SR_LAUNCH(embed_norm_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, (const bf16_t*)E, d, tok,
                        (const bf16_t*)g, eps, h, (bf16_t*)xn);
   else
-    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)E, d, tok,
+    SR_LAUNCH(embed_norm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)E, d, tok,
                        (const float*)g, eps, h, (float*)xn);
   SR_CHECK_LAUNCH();
 }
@@ -301,13 +301,13 @@ static void launch_add_norm(const float* part, int splits, int rows, int d, floa
   const int kv = (d4 + nt - 1) / nt;
   SR_REQUIRE(kv <= 4, 3, "d_model too large for add_norm");
   if (kv == 1)
-    hipLaunchKernelGGL((add_norm_kernel<T, 1>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+    SR_LAUNCH((add_norm_kernel<T, 1>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
                        (const T*)g, eps, (T*)xn);
   else if (kv == 2)
-    hipLaunchKernelGGL((add_norm_kernel<T, 2>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+    SR_LAUNCH((add_norm_kernel<T, 2>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
                        (const T*)g, eps, (T*)xn);
   else
-    hipLaunchKernelGGL((add_norm_kernel<T, 4>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
+    SR_LAUNCH((add_norm_kernel<T, 4>), dim3(rows), dim3(nt), 0, s, part, splits, rows, d, h,
                        (const T*)g, eps, (T*)xn);
   SR_CHECK_LAUNCH();
 }
@@ -369,10 +369,10 @@ void qkv_finalize(int dtype, const float* part, int splits, int rows, int hq, in
   if (rows <= 0) return;
   dim3 grid(rows, hq + 2 * hkv);
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(qkv_finalize_kernel<bf16_t>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
+    SR_LAUNCH(qkv_finalize_kernel<bf16_t>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
                        pos, qout, (bf16_t*)kdst, (bf16_t*)vdst, cap, t0);
   else
-    hipLaunchKernelGGL(qkv_finalize_kernel<float>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
+    SR_LAUNCH(qkv_finalize_kernel<float>, grid, dim3(64), 0, s, part, splits, rows, hq, hkv, hd, tab,
                        pos, qout, (float*)kdst, (float*)vdst, cap, t0);
   SR_CHECK_LAUNCH();
 }
@@ -401,10 +401,10 @@ void score_head(int dtype, const float* h, int d, int lr, int t0, const int32_t*
                 const void* g, const void* w, float eps, float* score, hipStream_t s) {
   if (rows <= 0) return;
   if (dtype == SR_BF16)
-    hipLaunchKernelGGL(score_head_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
+    SR_LAUNCH(score_head_kernel<bf16_t>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
                        (const bf16_t*)g, (const bf16_t*)w, eps, score);
   else
-    hipLaunchKernelGGL(score_head_kernel<float>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
+    SR_LAUNCH(score_head_kernel<float>, dim3(rows), dim3(256), 0, s, h, d, lr, t0, len,
                        (const float*)g, (const float*)w, eps, score);
   SR_CHECK_LAUNCH();
 }
@@ -422,7 +422,7 @@ __global__ void gather_tokens_kernel(const int32_t* __restrict__ store, int ld, 
 void gather_tokens(const int32_t* store, int ld, const int32_t* cand, const int32_t* len, int rows,
                    int t0, int lr, int32_t* tokens, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(gather_tokens_kernel, dim3(rows), dim3(256), 0, s, store, ld, cand, len, t0, lr, tokens);
+  SR_LAUNCH(gather_tokens_kernel, dim3(rows), dim3(256), 0, s, store, ld, cand, len, t0, lr, tokens);
   SR_CHECK_LAUNCH();
 }
 
@@ -434,7 +434,7 @@ __global__ void philox_fill_kernel(uint2 key, const uint4* __restrict__ ctr, int
 void philox_fill(uint64_t seed, const uint32_t* ctr, int n, uint32_t* out, hipStream_t s) {
   if (n <= 0) return;
   uint2 key = make_uint2((uint32_t)seed, (uint32_t)(seed >> 32));
-  hipLaunchKernelGGL(philox_fill_kernel, dim3((n + 255) / 256), dim3(256), 0, s, key,
+  SR_LAUNCH(philox_fill_kernel, dim3((n + 255) / 256), dim3(256), 0, s, key,
                      (const uint4*)ctr, n, (uint4*)out);
   SR_CHECK_LAUNCH();
 }

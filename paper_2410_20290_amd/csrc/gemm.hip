@@ -1334,7 +1334,7 @@ static void launch_bf16(const GemmArgs& g, int splits, int kps, const EpiArgs& e
                         hipStream_t s) {
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   dim3 grid = tile_grid((g.M + BM - 1) / BM, (g.N + BN - 1) / BN, splits);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, BK, WM, WN, PAIRED>), grid, dim3(NT), 0, s,
+  SR_LAUNCH((gemm_bf16_kernel<BM, BN, BK, WM, WN, PAIRED>), grid, dim3(NT), 0, s,
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N,
                      g.K, kps, e, part);
   SR_CHECK_LAUNCH();
@@ -1457,13 +1457,13 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     const int ncols = (g.paired ? 2 : 1) * g.N;
     SR_REQUIRE((size_t)g.M * ncols <= partial_cap, 5, "GEMM partial buffer too small");
     dim3 grid((ncols + 63) / 64, (g.M + 63) / 64);
-    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, (const float*)g.A, g.lda,
+    SR_LAUNCH(gemm_f32_kernel, grid, dim3(256), 0, s, (const float*)g.A, g.lda,
                        (const float*)g.B, g.ldb, g.pair_off, (int)g.paired, g.M, g.N, g.K, partial);
     SR_CHECK_LAUNCH();
     if (g.epi == EPI_PARTIAL) return 1;
     int64_t total = (int64_t)g.M * g.N;
     int blocks = (int)std::min<int64_t>((total + 255) / 256, 4096);
-    hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, partial, 1, g.M, g.N,
+    SR_LAUNCH(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, partial, 1, g.M, g.N,
                        (int)g.paired, e);
     SR_CHECK_LAUNCH();
     return 1;
@@ -1481,11 +1481,11 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   if (plan.stream && dma_offsets_fit(g)) {
     dim3 grid = tile_grid((g.M + plan.stream - 1) / plan.stream, (g.N + plan.stream_bn - 1) / plan.stream_bn, splits);
 #define SR_STREAM(BM, BN, WGM, WGN, NST, P, BK, ROT)                                                    \
-  hipLaunchKernelGGL((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, BK>), grid, dim3(256), 0, s,           \
+  SR_LAUNCH((gemm_stream_kernel<BM, BN, WGM, WGN, NST, P, BK>), grid, dim3(256), 0, s,           \
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, ROT, e, \
                      part)
 #define SR_RING(BM, BN, WGM, WGN, NA, NW, P, BK, ROT)                                                    \
-  hipLaunchKernelGGL((gemm_ring_kernel<BM, BN, WGM, WGN, NA, NW, P, BK>), grid, dim3(256), 0, s,          \
+  SR_LAUNCH((gemm_ring_kernel<BM, BN, WGM, WGN, NA, NW, P, BK>), grid, dim3(256), 0, s,          \
                      (const bf16_t*)g.A, g.lda, (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, ROT, e, \
                      part)
     // The paired (gate and up) projections start each tile at its own K
@@ -1520,17 +1520,17 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     const int bn_out = g.paired ? 64 : 128;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
     if (g.paired)
-      hipLaunchKernelGGL(gemm_dma3_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+      SR_LAUNCH(gemm_dma3_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
                          (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     else
-      hipLaunchKernelGGL(gemm_dma3_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+      SR_LAUNCH(gemm_dma3_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
                          (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     SR_CHECK_LAUNCH();
   } else if (plan.dma && dma_offsets_fit(g, 31)) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
 #define SR_DMA(P, R)                                                                                   \
-  hipLaunchKernelGGL((gemm_dma_kernel<P, R>), grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,        \
+  SR_LAUNCH((gemm_dma_kernel<P, R>), grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,        \
                      (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part)
     if (plan.dma_bring == 3) {
       if (g.paired) SR_DMA(true, 3);
@@ -1545,10 +1545,10 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
     const int bn_out = g.paired ? 128 : 256;
     dim3 grid = tile_grid((g.M + 255) / 256, (g.N + bn_out - 1) / bn_out, splits);
     if (g.paired)
-      hipLaunchKernelGGL(gemm_big_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+      SR_LAUNCH(gemm_big_kernel<true>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
                          (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     else
-      hipLaunchKernelGGL(gemm_big_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
+      SR_LAUNCH(gemm_big_kernel<false>, grid, dim3(256), 0, s, (const bf16_t*)g.A, g.lda,
                          (const bf16_t*)g.B, g.ldb, g.pair_off, g.M, g.N, g.K, kps, e, part);
     SR_CHECK_LAUNCH();
   } else if (g.paired) {
@@ -1563,7 +1563,7 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
   if (splits > 1 && g.epi != EPI_PARTIAL) {
     int64_t total = (int64_t)g.M * g.N;
     int blocks = (int)std::min<int64_t>((total + 255) / 256, 8192);
-    hipLaunchKernelGGL(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, g.M, g.N,
+    SR_LAUNCH(gemm_reduce_kernel, dim3(blocks), dim3(256), 0, s, part, splits, g.M, g.N,
                        (int)g.paired, e);
     SR_CHECK_LAUNCH();
   }

@@ -295,7 +295,11 @@ struct Model {
   const void* w2(int l) const { return wb(w->w2, (int64_t)l * m.d * m.ff); }
 };
 
-// Optional per-kernel-class timing with HIP events on the caller's stream.
+thread_local LaunchTiming* launch_timing = nullptr;
+
+// Optional per-kernel-class timing with HIP events on the caller's stream,
+// stamped by the kernels' own dispatch packets (SR_LAUNCH): a timed call
+// spans from its first kernel's start to its last kernel's end.
 struct Profiler {
   hipStream_t s = nullptr;
   bool active = false;
@@ -317,14 +321,14 @@ struct Profiler {
     for (auto& p : pool)
       for (hipEvent_t e : p) (void)hipEventDestroy(e);
   }
-  size_t mark() {
+  // the next unused event of the batch being recorded
+  size_t slot() {
     std::vector<hipEvent_t>& p = pool[cur];
     if (used == p.size()) {
       hipEvent_t e;
       SR_HIP(hipEventCreate(&e));
       p.push_back(e);
     }
-    SR_HIP(hipEventRecord(p[used], s));
     return used++;
   }
   // Waits for the launches of batch v (events of pool p) and accumulates
@@ -373,10 +377,17 @@ static void timed(const Ctx& c, int cls, double bytes, double flops, F&& launch)
     launch();
     return;
   }
-  const size_t a = p->mark();
-  launch();
-  const size_t b = p->mark();
-  p->recs.push_back({cls, a, b, bytes, flops});
+  const size_t a = p->slot(), b = p->slot();
+  LaunchTiming lt{p->pool[p->cur][a], p->pool[p->cur][b], false};
+  launch_timing = &lt;
+  try {
+    launch();
+  } catch (...) {
+    launch_timing = nullptr;
+    throw;
+  }
+  launch_timing = nullptr;
+  if (lt.started) p->recs.push_back({cls, a, b, bytes, flops});
 }
 
 // Projection launch.  decode: a generator decode projection (classed by
@@ -692,7 +703,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
   }
   prompt_prefill(c, G, L.rope_g, L.gpre);
   prompt_logits(c, G);
-  hipLaunchKernelGGL(init_state_kernel, dim3((N + 255) / 256), dim3(256), 0, s, N, L.st[0].cand,
+  SR_LAUNCH(init_state_kernel, dim3((N + 255) / 256), dim3(256), 0, s, N, L.st[0].cand,
                      L.st[0].len, L.st[0].done, L.cand_len, L.i_count, L.lp_sum);
   SR_CHECK_LAUNCH();
   out->sec_prefill = tph.stop();
@@ -761,7 +772,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
     int unfinished = 0;
     for (int i = 0; i < b; ++i) unfinished += h_done[i] == 0;
     State& st = L.st[cur];
-    hipLaunchKernelGGL(lens_kernel, dim3((b + 255) / 256), dim3(256), 0, s, st.len, b, L.cand_len,
+    SR_LAUNCH(lens_kernel, dim3((b + 255) / 256), dim3(256), 0, s, st.len, b, L.cand_len,
                        st.cand);
     SR_CHECK_LAUNCH();
     if (D == Lmax || unfinished == 0) {
@@ -853,7 +864,7 @@ static void generate(const sr_model* gen, const sr_model* rm, const int32_t* pro
         if (tr->round_accept) copy_d2h(tr->round_accept + (size_t)r * N, L.accept, sizeof(int32_t) * cnt, s);
       }
       ++r;
-      hipLaunchKernelGGL(compose_kernel, dim3((cnt2 + 255) / 256 + 1), dim3(256), 0, s, L.src_row,
+      SR_LAUNCH(compose_kernel, dim3((cnt2 + 255) / 256 + 1), dim3(256), 0, s, L.src_row,
                          L.src_row2, L.count2, L.src_tmp);
       SR_CHECK_LAUNCH();
       SR_HIP(hipMemcpyAsync(L.src_row, L.src_tmp, sizeof(int32_t) * std::max(cnt2, 1),
@@ -975,7 +986,7 @@ static void teacher_forced(const sr_model* gen, const sr_model* rm, const int32_
                           hipMemcpyDeviceToDevice, s));
   State st = L.st[0];
   for (int t = 1; t < len; ++t) {
-    hipLaunchKernelGGL(column_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, tokens, len, t - 1, rows,
+    SR_LAUNCH(column_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, tokens, len, t - 1, rows,
                        st.tok);
     SR_CHECK_LAUNCH();
     decode_step(c, G, st, rows, t, L.pool[0], pl.S[0] * gd.hkv * gd.hd, len);
@@ -1013,7 +1024,7 @@ static void reward_entry(const sr_model* gen, const sr_model* rm, const int32_t*
   // the responses become the token store; rows are their own candidates
   SR_HIP(hipMemcpy2DAsync(L.store, (size_t)pl.Lmax * 4, tokens, (size_t)max_len * 4, (size_t)max_len * 4,
                           rows, hipMemcpyDeviceToDevice, s));
-  hipLaunchKernelGGL(init_state_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, rows, L.st[0].cand,
+  SR_LAUNCH(init_state_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, rows, L.st[0].cand,
                      L.st[0].len, L.st[0].done, L.cand_len, L.i_count, L.lp_sum);
   SR_CHECK_LAUNCH();
   reward_rows(c, R, L.st[0].cand, lens, rows, max_len, scores);

@@ -241,7 +241,7 @@ void sample(const SampleArgs& a, hipStream_t s) {
   const int greedy = a.temperature == 0.0f;
   const float inv_t = greedy ? 1.0f : (float)(1.0 / (double)a.temperature);
   const uint2 key = make_uint2((uint32_t)a.seed, (uint32_t)(a.seed >> 32));
-  hipLaunchKernelGGL(sample_kernel, dim3(a.rows), dim3(kSampleThreads), 0, s, a.logits, a.row_stride,
+  SR_LAUNCH(sample_kernel, dim3(a.rows), dim3(kSampleThreads), 0, s, a.logits, a.row_stride,
                      a.vocab, a.cand, a.step, inv_t, greedy, key, a.next_tok, a.done, a.len, a.store,
                      a.store_ld, a.eos_id);
   SR_CHECK_LAUNCH();
@@ -289,7 +289,7 @@ __global__ void logprob_score_kernel(const float* __restrict__ lp_sum, const int
 void logprob_accumulate(const float* logits, int64_t row_stride, int rows, int vocab, const int32_t* cand,
                         const int32_t* tok, const int32_t* len, int step, float* lp_sum, hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(logprob_kernel, dim3(rows), dim3(256), 0, s, logits, row_stride, vocab, cand, tok, len, step,
+  SR_LAUNCH(logprob_kernel, dim3(rows), dim3(256), 0, s, logits, row_stride, vocab, cand, tok, len, step,
                      lp_sum);
   SR_CHECK_LAUNCH();
 }
@@ -297,7 +297,7 @@ void logprob_accumulate(const float* logits, int64_t row_stride, int rows, int v
 void logprob_scores(const float* lp_sum, const int32_t* cand, const int32_t* len, int rows, float* score,
                     hipStream_t s) {
   if (rows <= 0) return;
-  hipLaunchKernelGGL(logprob_score_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, lp_sum, cand, len, rows,
+  SR_LAUNCH(logprob_score_kernel, dim3((rows + 255) / 256), dim3(256), 0, s, lp_sum, cand, len, rows,
                      score);
   SR_CHECK_LAUNCH();
 }
