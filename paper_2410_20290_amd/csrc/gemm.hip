@@ -1105,8 +1105,8 @@ gemm_stream_kernel(const bf16_t* __restrict__ A, int lda, const bf16_t* __restri
 // copies of a step go out activation rows first, then weight rows; at step
 // t the wait leaves in flight only the weight copies issued after the
 // activation rows of step t (those of step t + NW - 2).  `rot` > 0 starts
-// tile n at K step (n rot) mod nk and wraps, which spreads the HBM rows that
-// the tiles stream at one time over more banks.  Fragment reads and the MFMA
+// tile n at K step (n rot) mod nk and wraps, so the tiles stream their rows
+// at staggered K offsets instead of in lockstep.  Fragment reads and the MFMA
 // tiling are those of gemm_stream_kernel; BK 128 or 256 (a copy instruction
 // then moves 4 rows of 256 bytes or 2 rows of 512 bytes).
 template <int BM, int BN, int WGM, int WGN, int NA, int NW, bool PAIRED, int BK>
