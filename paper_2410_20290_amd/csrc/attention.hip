@@ -562,13 +562,13 @@ decode_wave_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
 // key block costs the same MFMAs as one row's tail block but serves R rows.
 // Work-group = (split, KV head, row group), NW = R WPR waves: wave w takes
 // an even share of the prefix blocks (all 16 columns) and one WPR-th of row
-// (w mod R)'s tail blocks (its G columns are the ones kept); both runs
-// stream as in decode_wave_kernel (K into registers, V copied to the wave's
-// LDS double buffer and read back transposed).  The waves' prefix partials
-// and tail partials are merged per column through LDS; the work-group
-// writes the output or, with several splits, its partial slot.  Fused QKV
-// finalize: the wave holding a row's last tail block writes the row's
-// newest K/V first.
+// (w mod R)'s tail blocks (the other rows' columns masked), all streamed as
+// one run as in decode_wave_kernel (K into registers, V copied to the wave's
+// LDS double buffer and read back transposed), with one softmax state per
+// column.  The waves' partials are merged per column through LDS; the
+// work-group writes the output or, with several splits, its partial slot.
+// Fused QKV finalize: the wave holding a row's last tail block writes the
+// row's newest K/V first.
 template <int HD, int G, int WPR>
 __global__ void __launch_bounds__(64 * (16 / G) * WPR)
 decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre, const bf16_t* __restrict__ vpre,
@@ -584,7 +584,7 @@ decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre
   constexpr int INFLIGHT = 2 * KS + NDMA;
   static_assert(HD == 64 || HD == 128, "head_dim");
   static_assert(G == 2 || G == 4 || G == 8, "query heads per KV head");
-  static_assert(NW <= 8 && NW * (16 + G) * (HD + 2) * 4 <= NW * 2 * VB * 2, "merge area within the V buffers");
+  static_assert(NW <= 8 && NW * 16 * (HD + 2) * 4 <= NW * 2 * VB * 2, "merge area within the V buffers");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NW * 2 * VB];
   const int split = blockIdx.x, h = blockIdx.y, grp = blockIdx.z;
   const int lane = threadIdx.x & 63;
@@ -700,7 +700,14 @@ decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre
     }
   };
   const int kr0 = 4 * fg + (fr >> 2), kr1 = kr0 + 16;
-  auto compute = [&](int k0, int k1, const uint4 (&kr)[2][KS], int buf, f32x4 (&o)[DT], float& m, float& l) {
+  f32x4 o[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f;
+  // A block of a row's tail serves only that row's G columns: the other
+  // columns' scores are masked, so prefix and tail blocks share one
+  // softmax state per column.
+  auto compute = [&](int k0, int k1, bool tail, const uint4 (&kr)[2][KS], int buf) {
     f32x4 st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -711,11 +718,12 @@ decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre
                                                         0);
     }
     const int jb = k0 + 4 * fg;
+    const int kend = tail && fr / G != rr ? k0 : k1;   // masked columns: no key
     float sv[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      sv[i] = jb + i < k1 ? st[0][i] : -INFINITY;
-      sv[4 + i] = jb + 16 + i < k1 ? st[1][i] : -INFINITY;
+      sv[i] = jb + i < kend ? st[0][i] : -INFINITY;
+      sv[4 + i] = jb + 16 + i < kend ? st[1][i] : -INFINITY;
     }
     float mt = sv[0];
 #pragma unroll
@@ -745,76 +753,61 @@ decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(tr16_pair(lo, hi), pf, o[dt], 0, 0, 0);
     }
   };
-  // one run of nb blocks starting at key b0 (block ends clamped to b1),
-  // the next block's loads in flight while a block is computed
-  auto run = [&](const bf16_t* kb_, const bf16_t* vb_, int b0, int b1, f32x4 (&o)[DT], float& m, float& l) {
-    const int nb = (b1 - b0 + 31) >> 5;
-    if (nb <= 0) return;
+  // The wave's blocks: its prefix share [pk0, pk1) of (kp, vp), then its
+  // share [tk0, tk1) of row rr's tail in (kt, vt); one pipeline over both,
+  // the next block's loads in flight while a block is computed.
+  const int pk0 = 32 * pb0, pk1 = min(32 * pb1, P);
+  const int tk0 = 32 * tb0, tk1 = min(32 * tb1, lt);
+  const int np = pk1 > pk0 ? (pk1 - pk0 + 31) >> 5 : 0;
+  const int nb = np + (tk1 > tk0 ? (tk1 - tk0 + 31) >> 5 : 0);
+  auto key0 = [&](int b) { return b < np ? pk0 + 32 * b : tk0 + 32 * (b - np); };
+  auto keyend = [&](int b) { return b < np ? min(pk0 + 32 * b + 32, pk1) : min(tk0 + 32 * (b - np) + 32, tk1); };
+  auto fetch = [&](int b, uint4 (&kr)[2][KS], int buf) {
+    const bool tail = b >= np;
+    load_k(tail ? kt : kp, key0(b), keyend(b), kr);
+    copy_v(tail ? vt : vp, key0(b), keyend(b), buf);
+  };
+  if (nb > 0) {
     uint4 ka[2][KS], kb[2][KS];
-    load_k(kb_, b0, min(b0 + 32, b1), ka);
-    copy_v(vb_, b0, min(b0 + 32, b1), 0);
+    fetch(0, ka, 0);
     for (int b = 0; b < nb; b += 2) {
-      const int s0 = b0 + 32 * b, s1 = s0 + 32, s2 = s0 + 64;
       if (b + 1 < nb) {
-        load_k(kb_, s1, min(s1 + 32, b1), kb);
-        copy_v(vb_, s1, min(s1 + 32, b1), 1);
+        fetch(b + 1, kb, 1);
         vm_wait<INFLIGHT>();
       } else {
         vm_wait<0>();
       }
-      compute(s0, min(s0 + 32, b1), ka, 0, o, m, l);
+      compute(key0(b), keyend(b), b >= np, ka, 0);
       if (b + 1 < nb) {
         asm volatile("" ::: "memory");
         if (b + 2 < nb) {
-          load_k(kb_, s2, min(s2 + 32, b1), ka);
-          copy_v(vb_, s2, min(s2 + 32, b1), 0);
+          fetch(b + 2, ka, 0);
           vm_wait<INFLIGHT>();
         } else {
           vm_wait<0>();
         }
-        compute(s1, min(s1 + 32, b1), kb, 1, o, m, l);
+        compute(key0(b + 1), keyend(b + 1), b + 1 >= np, kb, 1);
         asm volatile("" ::: "memory");
       }
     }
-  };
+  }
 
-  f32x4 op[DT], ot[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) op[dt] = ot[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mp = -INFINITY, lp = 0.f, mtl = -INFINITY, ltl = 0.f;
-  run(kp, vp, 32 * pb0, min(32 * pb1, P), op, mp, lp);
-  run(kt, vt, 32 * tb0, min(32 * tb1, lt), ot, mtl, ltl);
-
-  // merge: per column c (row grp R + c / G, head h G + c % G) the prefix
-  // partials of all waves and the tail partials of the row's WPR waves
-  lp += __shfl_xor(lp, 16, 64);
-  lp += __shfl_xor(lp, 32, 64);
-  ltl += __shfl_xor(ltl, 16, 64);
-  ltl += __shfl_xor(ltl, 32, 64);
+  // merge: per column c (row grp R + c / G, head h G + c % G) the partials
+  // of all waves (prefix shares, and the tail shares of the row's waves)
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
   __syncthreads();
   constexpr int SL = HD + 2;
-  float* sp_ = reinterpret_cast<float*>(lds);   // [NW][16][SL] prefix partials
-  float* st_ = sp_ + NW * 16 * SL;               // [NW][G][SL] tail partials (the wave's row)
+  float* sp_ = reinterpret_cast<float*>(lds);   // [NW][16][SL]
   {
     float* w = sp_ + (wave * 16 + fr) * SL;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[dt * 16 + 4 * fg + i] = op[dt][i];
+      for (int i = 0; i < 4; ++i) w[dt * 16 + 4 * fg + i] = o[dt][i];
     if (fg == 0) {
-      w[HD] = mp;
-      w[HD + 1] = lp;
-    }
-    if (fr / G == rr) {
-      float* wt = st_ + (wave * G + fr % G) * SL;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) wt[dt * 16 + 4 * fg + i] = ot[dt][i];
-      if (fg == 0) {
-        wt[HD] = mtl;
-        wt[HD + 1] = ltl;
-      }
+      w[HD] = m;
+      w[HD + 1] = l;
     }
   }
   __syncthreads();
@@ -825,20 +818,11 @@ decode_group_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < NW; ++w) M = fmaxf(M, sp_[(w * 16 + c) * SL + HD]);
-#pragma unroll
-    for (int w = c / G; w < NW; w += R) M = fmaxf(M, st_[(w * G + g) * SL + HD]);
     float L = 0.f, A = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
       for (int w = 0; w < NW; ++w) {
         const float* ws = sp_ + (w * 16 + c) * SL;
-        const float cf = exp2_or_zero(ws[HD] - M);
-        L += ws[HD + 1] * cf;
-        A += ws[d] * cf;
-      }
-#pragma unroll
-      for (int w = c / G; w < NW; w += R) {
-        const float* ws = st_ + (w * G + g) * SL;
         const float cf = exp2_or_zero(ws[HD] - M);
         L += ws[HD + 1] * cf;
         A += ws[d] * cf;
