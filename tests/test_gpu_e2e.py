@@ -178,13 +178,14 @@ def test_bf16_audit(name):
     for k in (0, c.n // 2, c.n - 1):
         ref = g.logits(list(prompt) + list(toks[k]))[len(prompt) - 1: len(prompt) - 1 + c.tau]
         assert np.abs(lg[k] - ref).max() <= tol(c) * np.abs(ref).max()
-    # (3) partial rewards of every cut, recomputed by the oracle (the rounds
-    # after the first score through the reward model's cached K/V)
+    # (3) partial rewards of every candidate at every cut, recomputed by the
+    # oracle (the rounds after the first score through the reward model's
+    # cached K/V), within the tolerance of the cut's whole reward vector
     assert len(rounds) >= 2
     for (L0, b0, K0, cand0, sc0, acc0) in rounds:
-        js = sorted({0, min(7, b0 - 1), b0 - 1})
-        refs = np.array([orm.score(list(prompt) + t["all_tokens"][cand0[j], :L0].tolist()) for j in js])
-        assert np.abs(sc0[js] - refs).max() <= tol(c) * np.abs(refs).max(), (L0, js)
+        refs = np.array([orm.score(list(prompt) + t["all_tokens"][cand0[j], :L0].tolist()) for j in range(b0)])
+        err = np.abs(sc0 - refs)
+        assert err.max() <= tol(c) * np.abs(refs).max(), (L0, int(err.argmax()))
     # (4) final rewards of I, recomputed by the oracle
     fs = t["final_scores"]
     mem = [k for k in range(c.n) if not np.isnan(fs[k])]
