@@ -1380,6 +1380,13 @@ GemmPlan gemm_plan(int dtype, int M, int N, int K, bool paired) {
   p.stream = 0;
   p.stream_bn = 0;
   if (dtype != SR_BF16) return p;
+  if (M > 64 && M <= 112 && !paired && N > 65536 && K % 128 == 0) {
+    // The LM head at 65-112 rows: 112 x 128 tiles, one per work-group, with
+    // the separate activation and weight rings (enough tiles without split).
+    p.stream = 112;
+    p.stream_bn = 128;
+    return p;
+  }
   if (M <= kStreamMaxRows && K % 128 == 0 && (M <= 64 || N <= 65536)) {
     // One round of work-groups (one per CU): split K by the largest power of
     // two that keeps the grid within 256 and each split a multiple of 128.
@@ -1508,6 +1515,7 @@ int gemm(const GemmArgs& g, float* partial, size_t partial_cap, hipStream_t s) {
       // side over the columns (less padding than 128 rows); paired: two
       // weight stages in flight beside the activation ring
       if (g.paired) SR_RING(112, 64, 1, 4, 2, 3, true, 128, kTileRot);
+      else if (plan.stream_bn == 128) SR_RING(112, 128, 1, 4, 2, 3, false, 128, 0);
       else SR_STREAM(112, 64, 1, 4, 3, false, 128, 0);
     } else {
       if (g.paired) SR_RING(128, 64, 2, 2, 2, 3, true, 128, kTileRot);

@@ -27,6 +27,8 @@ SHAPES = [(1, 64, 64), (17, 100, 128), (33, 1000, 512), (100, 384, 4096), (129, 
           (70, 2000, 8192), (103, 4096, 14336),
           # 65-112 rows with 2 to 6 K steps of 256 per work-group
           (97, 4150, 512), (65, 4200, 768), (100, 4096, 4096), (112, 4100, 1280), (77, 4200, 1536),
+          # 65-112 rows, more than 65536 columns (the LM head's tiles), ragged N
+          (103, 66000, 384), (70, 65601, 128),
           # paired few-row tiles with 512-byte rows per copy (K steps of 256), ragged N
           (21, 4100, 2048),
           # thousands of rows, ragged in M and N, ten K steps (the 256 x 256 tile)
