@@ -38,6 +38,34 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def device_clocks(libhandle):
+    """Peak engine and memory clocks the HIP runtime reports for device 0
+    (MHz), with the engine clock the counters measured under the matrix-core
+    bound reward-model GEMMs (profiles/mfma_batched_gemms.json) for context.
+    The runtime is reached through the library's handle (its dependency
+    scope), so the process keeps the one HIP runtime it already has."""
+    import ctypes
+    out = {}
+    try:
+        get = libhandle.hipDeviceGetAttribute
+    except AttributeError:
+        get = None
+    if get is not None:
+        v = ctypes.c_int()
+        # hipDeviceAttributeClockRate = 5, hipDeviceAttributeMemoryClockRate = 60 (kHz)
+        for key, attr in (("sclk_peak_mhz", 5), ("mclk_peak_mhz", 60)):
+            if get(ctypes.byref(v), attr, 0) == 0:
+                out[key] = v.value // 1000
+    try:
+        with open(os.path.join(ROOT, "profiles", "mfma_batched_gemms.json")) as f:
+            d = json.load(f)
+        out["sclk_under_mfma_load_ghz"] = d["reward_model_32768_rows"]["w13"]["sustained_clock_ghz"]
+        out["sclk_under_mfma_load_source"] = "profiles/mfma_batched_gemms.json (GRBM_GUI_ACTIVE per XCD / launch time)"
+    except (OSError, KeyError, ValueError):
+        pass
+    return out or None
+
+
 def roofline_of(name, k, dtype):
     bound, unit = BOUNDS[name]
     if k["sec"] <= 0:
@@ -244,7 +272,7 @@ def counter_workload(cfg, gen, rm, prompt, case="all"):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="8b_bf16")
     ap.add_argument("--alpha", type=float, default=None)
@@ -469,6 +497,7 @@ def main():
                          "at larger N on several GPUs and is not comparable to speedup_vs_alpha0 (alpha=0 at the "
                          "same N on one GPU).",
         "cpu_baseline": cpu,
+        "clocks": device_clocks(sr.lib()),
     }
     print(json.dumps(line), flush=True)
 
