@@ -871,7 +871,7 @@ static int decode_kps(int rows, int hkv, int keys) {
 // Waves decode_wave_kernel aims at over the whole grid.
 constexpr int kWaveTarget = 2048;
 
-template <int HD, int G, bool PREFIX_ONLY>
+template <int HD, int G, bool PREFIX_ONLY, int QB>
 __global__ void prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
                                          const bf16_t* __restrict__ vown, int rows, int lr, int cap, int t0, int hq,
@@ -984,7 +984,7 @@ static void launch_decode(const DecodeAttnArgs& a, hipStream_t s) {
   // runs last: the tails leave partial slots and it folds them into its own
   // result, so no merge pass is needed.
   auto prefix_pass = [&](int tsplits) {
-    SR_LAUNCH((prefill_attn_mfma_kernel<128, G, true>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
+    SR_LAUNCH((prefill_attn_mfma_kernel<128, G, true, 1>), dim3((a.rows + 15) / 16, a.hkv, 1), dim3(64 * G), 0, s,
                        a.q, (const bf16_t*)a.kpre, (const bf16_t*)a.vpre, a.P, nullptr, nullptr, 1, a.rows, 0, 0, a.hq,
                        a.hkv, (bf16_t*)a.out, qscale, a.part, tsplits);
     SR_CHECK_LAUNCH();
@@ -1265,13 +1265,14 @@ constexpr int PF_KT = 32;            // keys per tile
 // and left part_splits partial slots per (row, query head) in `part`
 // (unnormalised output, running max, sum); the work-group folds them into
 // its own result by log-sum-exp and writes the attention output.
-template <int HD, int G, bool PREFIX_ONLY>
-__global__ void __launch_bounds__(64 * G)
+template <int HD, int G, bool PREFIX_ONLY, int QB>
+__global__ void __launch_bounds__(64 * G * QB)
 prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__ kpre,
                          const bf16_t* __restrict__ vpre, int P, const bf16_t* __restrict__ kown,
                          const bf16_t* __restrict__ vown, int rows, int lr, int cap, int t0, int hq, int hkv,
                          bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
-  constexpr int NT = 64 * G;
+  constexpr int NT = 64 * G * QB;
+  static_assert(!PREFIX_ONLY || QB == 1, "the prefix pass takes one query block per work-group");
   constexpr int KS = HD / 32, DT = HD / 16, CPK = HD / 8;
   constexpr int PF_KROW = HD + 8;    // K tile row (bf16), padded
   constexpr int PF_VROW = HD + 16;   // V tile row (bf16), padded: the 8-byte transpose reads of a
@@ -1283,23 +1284,26 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   // to the 8 XCDs: XCD x takes the consecutive logical blocks
   // [x C, (x + 1) C), ordered query block fastest, so the query blocks that
   // read the same row's keys share one L2.
-  int qb, h, row;
+  int qb0, h, row;
   if constexpr (PREFIX_ONLY) {
-    qb = blockIdx.x;
+    qb0 = blockIdx.x;
     h = blockIdx.y;
     row = 0;
   } else {
-    const int nqb = (lr + 15) / 16, total = nqb * hkv * rows;
+    const int ngq = ((lr + 15) / 16 + QB - 1) / QB, total = ngq * hkv * rows;
     const int per_xcd = (total + 7) / 8;
     const int pid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     if (pid >= total) return;
-    qb = pid % nqb;
-    h = (pid / nqb) % hkv;
-    row = pid / (nqb * hkv);
+    qb0 = (pid % ngq) * QB;
+    h = (pid / ngq) % hkv;
+    row = pid / (ngq * hkv);
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int fr = lane & 15, fg = lane >> 4;
-  const int qh = h * G + wave;
+  // wave w: query head h G + w % G of query block qb0 + w / G (the QB
+  // blocks of a work-group share every staged K/V tile)
+  const int qb = qb0 + wave / G;
+  const int qh = h * G + wave % G;
   const int t = qb * 16 + fr;              // this lane's query (as B column / C column)
   const bool qvalid = t < lr;
   // Q^T fragments: lane holds Q[t][32 s + 8 fg .. +8] for k-step s (scaled,
@@ -1327,7 +1331,8 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f;
-  const int tlast = min(lr, (qb + 1) * 16) - 1;
+  // keys of the work-group's last query (its waves' masks cut the rest)
+  const int tlast = min(lr, (qb0 + QB) * 16) - 1;
   const int nkeys = PREFIX_ONLY ? P : P + t0 + tlast + 1;
   const bf16_t* kp = kpre + (int64_t)h * P * HD;
   const bf16_t* vp = vpre + (int64_t)h * P * HD;
@@ -1490,13 +1495,17 @@ static void prefill_by_hd(const PrefillAttnArgs& a, hipStream_t s) {
   }
 }
 
+// Waves per prefill work-group: G query heads x QB query blocks of 16.
+constexpr int kPrefillWaves = 8;
+
 template <int HD, int G>
 static void launch_prefill_mfma(const PrefillAttnArgs& a, hipStream_t s) {
   const float qscale = kLog2e / sqrtf((float)HD);
-  const int64_t total = (int64_t)((a.lr + 15) / 16) * a.hkv * a.rows;
+  constexpr int QB = kPrefillWaves / G;   // query blocks per work-group
+  const int64_t total = (int64_t)(((a.lr + 15) / 16 + QB - 1) / QB) * a.hkv * a.rows;
   SR_REQUIRE(total <= (int64_t)INT32_MAX - 8, SR_ERR_UNSUPPORTED, "prefill attention grid too large");
   dim3 grid((unsigned)(8 * ((total + 7) / 8)));
-  SR_LAUNCH((prefill_attn_mfma_kernel<HD, G, false>), grid, dim3(64 * G), 0, s, a.q, (const bf16_t*)a.kpre,
+  SR_LAUNCH((prefill_attn_mfma_kernel<HD, G, false, QB>), grid, dim3(64 * G * QB), 0, s, a.q, (const bf16_t*)a.kpre,
                      (const bf16_t*)a.vpre, a.P, (const bf16_t*)a.kown, (const bf16_t*)a.vown, a.rows, a.lr, a.cap,
                      a.t0, a.hq, a.hkv, (bf16_t*)a.out, qscale, nullptr, 0);
   SR_CHECK_LAUNCH();
