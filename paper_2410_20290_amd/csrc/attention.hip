@@ -16,9 +16,10 @@
 //                        the one-query-head-per-KV-head case at 128+ rows.
 // Online softmax in base 2; split partials are merged by log-sum-exp.
 //
-// Prefill (reward-model scoring, prompt): a work-group owns 16 queries of
-// one row and one KV head (MFMA flash attention, bf16 head_dim 64/128), or a
-// block of queries on the vector ALU with K/V staged in LDS as fp32.
+// Prefill (reward-model scoring, prompt): a work-group owns 8 / G blocks of
+// 16 queries of one row and one KV head (MFMA flash attention, bf16
+// head_dim 64/128), or a block of queries on the vector ALU with K/V staged
+// in LDS as fp32.
 #include <algorithm>
 #include <mutex>
 
@@ -1242,11 +1243,11 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 
 // --------------------------------------------------------- prefill (MFMA)
 // bf16 flash attention with v_mfma_f32_16x16x32_bf16, head_dim 64 or 128.
-// Work-group = one row, one KV head, 16 queries; wave w computes query head
-// (kvh * G + w) for those queries, so the G waves share every K/V tile
-// staged in LDS (32 keys).  (Two or four 16-query blocks per wave reuse a
-// tile more but hold too many registers for more than one or two
-// work-groups per SIMD, and measured slower.)
+// Work-group = one row, one KV head, QB blocks of 16 queries; wave w
+// computes query head (kvh * G + w % G) for query block w / G, so the G QB
+// waves share every K/V tile staged in LDS (32 keys).  (Two or four 16-query
+// blocks per wave instead reuse a tile more but hold too many registers for
+// more than one or two work-groups per SIMD, and measured slower.)
 //   S^T = K Q^T   (keys x queries): lane l holds keys 4(l/16)+i (+16 for the
 //                 second key tile) of query l%16, so the online-softmax state
 //                 of a query lives in one lane group (max/sum over l/16).
