@@ -94,9 +94,10 @@ PREFILL_CASES = [
     # dtype, hd, hq, hkv, rows, P, t0, lr, cap
     ("bf16", 128, 32, 8, 3, 40, 37, 29, 70),      # matrix-core kernel, ragged tiles
     ("bf16", 128, 32, 8, 2, 256, 128, 100, 636),  # 8B shapes: second scoring round
-    ("bf16", 128, 32, 8, 2, 256, 0, 128, 128),    # 8B shapes: first scoring round (64-query blocks)
-    ("bf16", 128, 32, 8, 2, 7, 45, 130, 200),     # 64-query blocks, ragged last block
-    ("bf16", 64, 32, 8, 2, 30, 3, 150, 160),      # head_dim 64, 64-query blocks
+    ("bf16", 128, 32, 8, 2, 256, 0, 128, 128),    # 8B shapes: first scoring round (two 16-query blocks a work-group)
+    ("bf16", 128, 32, 8, 2, 7, 45, 130, 200),     # ragged last block, last work-group with one block
+    ("bf16", 64, 32, 8, 2, 30, 3, 150, 160),      # head_dim 64
+    ("bf16", 128, 16, 8, 2, 20, 5, 70, 80),       # 2 query heads per KV head: 4 blocks a work-group, 5 blocks
     ("bf16", 128, 8, 8, 2, 0, 16, 33, 49),
     ("bf16", 128, 16, 2, 2, 17, 0, 50, 64),
     ("bf16", 128, 32, 8, 1, 5, 0, 1, 1),
