@@ -1245,7 +1245,7 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 // bf16 flash attention with v_mfma_f32_16x16x32_bf16, head_dim 64 or 128.
 // Work-group = one row, one KV head, QB blocks of 16 queries; wave w
 // computes query head (kvh * G + w % G) for query block w / G, so the G QB
-// waves share every K/V tile staged in LDS (32 keys).  (Two or four 16-query
+// waves share every K/V tile staged in LDS.  (Two or four 16-query
 // blocks per wave instead reuse a tile more but hold too many registers for
 // more than one or two work-groups per SIMD, and measured slower.)
 //   S^T = K Q^T   (keys x queries): lane l holds keys 4(l/16)+i (+16 for the
@@ -1256,9 +1256,10 @@ prefill_attn_kernel(const float* __restrict__ q, const T* __restrict__ kpre, con
 //                 S^T values (keys 4g..4g+3 of tile 0, then of tile 1); the A
 //                 operand comes from the V tile, staged row by row like K, by
 //                 two LDS transpose reads.
-// The next 32-key tile is fetched into registers while the current one is
-// computed.
-constexpr int PF_KT = 32;            // keys per tile
+// Tiles of 64 keys (32 in the prefix pass) staged in LDS, computed 32 keys
+// at a time; the next tile is fetched into registers while the current one
+// is computed.
+constexpr int PF_KT = 64;            // keys per staged tile (prefill form)
 
 // PREFIX_ONLY: the decode rows' attention over the shared prompt prefix.
 // The 16 "queries" of a work-group are 16 decode rows (lr = rows, one
@@ -1274,13 +1275,16 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
                          bf16_t* __restrict__ out, float qscale, float* __restrict__ part, int part_splits) {
   constexpr int NT = 64 * G * QB;
   static_assert(!PREFIX_ONLY || QB == 1, "the prefix pass takes one query block per work-group");
+  // keys per staged tile: 64 for the prefill form (its work-groups have
+  // eight waves to fetch them), 32 for the prefix pass (G waves)
+  constexpr int KT = PREFIX_ONLY ? 32 : PF_KT;
   constexpr int KS = HD / 32, DT = HD / 16, CPK = HD / 8;
   constexpr int PF_KROW = HD + 8;    // K tile row (bf16), padded
   constexpr int PF_VROW = HD + 16;   // V tile row (bf16), padded: the 8-byte transpose reads of a
                                      // half wave (eight rows) fall on distinct banks
   static_assert(HD == 64 || HD == 128, "head_dim");
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[PF_KT * PF_KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[PF_KT * PF_VROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * PF_KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[KT * PF_VROW];
   // The prefill form runs a 1-D grid of 8 C work-groups, dealt round-robin
   // to the 8 XCDs: XCD x takes the consecutive logical blocks
   // [x C, (x + 1) C), ordered query block fastest, so the query blocks that
@@ -1340,7 +1344,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   const bf16_t* ko = PREFIX_ONLY ? kp : kown + ((int64_t)row * hkv + h) * cap * HD;
   const bf16_t* vo = PREFIX_ONLY ? vp : vown + ((int64_t)row * hkv + h) * cap * HD;
   // a tile is 32 keys x CPK chunks of 8 dims; thread chunks c = tid + NT i
-  constexpr int CPT = (PF_KT * CPK + NT - 1) / NT;
+  constexpr int CPT = (KT * CPK + NT - 1) / NT;
   uint4 kreg[CPT], vreg[CPT];
   auto fetch = [&](int kb) {
 #pragma unroll
@@ -1348,7 +1352,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       const int c = threadIdx.x + NT * i;
       const int key = kb + c / CPK, cc = c % CPK;
       kreg[i] = vreg[i] = make_uint4(0, 0, 0, 0);
-      if (c < PF_KT * CPK && key < nkeys) {
+      if (c < KT * CPK && key < nkeys) {
         const bf16_t* kr = key < P ? kp + (int64_t)key * HD : ko + (int64_t)(key - P) * HD;
         const bf16_t* vr = key < P ? vp + (int64_t)key * HD : vo + (int64_t)(key - P) * HD;
         kreg[i] = *reinterpret_cast<const uint4*>(kr + cc * 8);
@@ -1359,9 +1363,10 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
   // Lane i of a group names dims dt 16 + 4 (i & 3) .. + 3 of key
   // 4 fg + (i >> 2) (and 16 keys on), so it receives dim dt 16 + i of keys
   // 4 fg .. + 3 (and 16 + 4 fg .. + 3): the A operand rows of O^T += V^T P^T
-  const bf16_t* vb = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
-  // the staged tile of keys kb .. kb + 31
-  auto compute = [&](int kb) {
+  const bf16_t* vb0 = &Vs[(4 * fg + (fr >> 2)) * PF_VROW + 4 * (fr & 3)];
+  // the staged tile's keys kb .. kb + 31, at tile row r0
+  auto compute = [&](int kb, int r0) {
+    const bf16_t* vb = vb0 + r0 * PF_VROW;
     // S^T for key tiles 0 (keys kb..kb+15) and 1 (kb+16..kb+31)
     f32x4 st[2];
 #pragma unroll
@@ -1369,7 +1374,7 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
       st[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(kt * 16 + fr) * PF_KROW + 32 * s + 8 * fg]);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&Ks[(r0 + kt * 16 + fr) * PF_KROW + 32 * s + 8 * fg]);
         st[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[s], st[kt], 0, 0, 0);
       }
     }
@@ -1411,20 +1416,21 @@ prefill_attn_mfma_kernel(const float* __restrict__ q, const bf16_t* __restrict__
     }
   };
   fetch(0);
-  for (int kb = 0; kb < nkeys; kb += PF_KT) {
+  for (int kb = 0; kb < nkeys; kb += KT) {
     // stage K [key][dim] and V [key][dim]
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = threadIdx.x + NT * i;
-      if (PF_KT * CPK % NT == 0 || c < PF_KT * CPK) {
+      if (KT * CPK % NT == 0 || c < KT * CPK) {
         const int j = c / CPK, cc = c % CPK;
         *reinterpret_cast<uint4*>(&Ks[j * PF_KROW + cc * 8]) = kreg[i];
         *reinterpret_cast<uint4*>(&Vs[j * PF_VROW + cc * 8]) = vreg[i];
       }
     }
     lds_barrier();
-    if (kb + PF_KT < nkeys) fetch(kb + PF_KT);
-    compute(kb);
+    if (kb + KT < nkeys) fetch(kb + KT);
+    compute(kb, 0);
+    if (KT == 64 && kb + 32 < nkeys) compute(kb + 32, 32);
     lds_barrier();
   }
   if (qvalid) {
